@@ -29,12 +29,13 @@ method's invariants in the tests.
 """
 from .weights import OracleModel, load_blob
 from .dit import (timestep_frequencies, timestep_embedding, modulation_table, patchify,
-                  unpatchify, layer_norm, gelu_tanh, silu, attention, forward_one, velocity)
+                  unpatchify, layer_norm, gelu_tanh, silu, attention, residual_one, forward_one,
+                  velocity)
 from .stream import euler, stream_step, run_stream, sequential_sample
 
 __all__ = [
     "OracleModel", "load_blob", "timestep_frequencies", "timestep_embedding",
     "modulation_table", "patchify", "unpatchify", "layer_norm", "gelu_tanh", "silu",
-    "attention", "forward_one", "velocity", "euler", "stream_step", "run_stream",
+    "attention", "residual_one", "forward_one", "velocity", "euler", "stream_step", "run_stream",
     "sequential_sample",
 ]

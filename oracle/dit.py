@@ -127,32 +127,55 @@ def modulation_table(m, t, dtype=np.float32):
     return np.concatenate(parts)
 
 
+def block_forward(m, b, h, s, ctx=None, trace=None):
+    """One adaLN block on the residual stream h [N, D] of one sample (s = SiLU(c)).
+    If `trace` is a dict, the block's intermediates are stored in it."""
+    D = m.D
+    mod = linear(s, b["W_mod"], b["b_mod"]).reshape(6, D)
+    shift1, scale1, gate1, shift2, scale2, gate2 = mod
+    a = layer_norm(h) * (1.0 + scale1) + shift1
+    qkv = linear(a, b["W_qkv"], b["b_qkv"])
+    q, k, v = qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:]
+    o = attention(q, k, v, m.heads)
+    h = h + gate1 * linear(o, b["W_o"], b["b_o"])
+    if trace is not None:
+        trace.update(ln1=a, q=q, k=k, v=v, attn=o, h_attn=h)
+    if m.has_cross:
+        if ctx is None:
+            raise ValueError("network has cross-attention: ctx is required")
+        qx = linear(layer_norm(h), b["W_qx"], b["b_qx"])
+        kv = linear(np.asarray(ctx, dtype=h.dtype), b["W_kvx"], b["b_kvx"])
+        ox = attention(qx, kv[:, :D], kv[:, D:], m.heads)
+        h = h + linear(ox, b["W_ox"], b["b_ox"])
+        if trace is not None:
+            trace.update(cross_q=qx, cross_attn=ox, h_cross=h)
+    a = layer_norm(h) * (1.0 + scale2) + shift2
+    f = gelu_tanh(linear(a, b["W_fc1"], b["b_fc1"]))
+    h = h + gate2 * linear(f, b["W_fc2"], b["b_fc2"])
+    if trace is not None:
+        trace.update(ln2=a, mlp=f, h_out=h)
+    return h
+
+
+def residual_one(m, x, t, ctx=None, blocks=None, dtype=np.float32, trace=None):
+    """Residual stream h [N, D] of ONE latent after the patch embedding and the first
+    `blocks` blocks (all blocks if None); `s` = SiLU(c) is returned alongside. With a
+    `trace` dict, the intermediates of the last block run are stored in it."""
+    m = m if dtype == np.float32 else m.astype(dtype)
+    x = np.asarray(x, dtype=dtype)
+    s = conditioning(m, t, dtype)
+    h = linear(patchify(x, m.p), m.top["W_pe"], m.top["b_pe"]) + m.top["pos"]
+    for b in m.blocks[:blocks]:
+        h = block_forward(m, b, h, s, ctx, trace)
+    return h, s
+
+
 def forward_one(m, x, t, ctx=None, dtype=np.float32):
     """v = F(x, t) for ONE latent x [C, H, W] at time t; ctx [ctx_len, ctx_dim] if the
     network has cross-attention. Returns v [C, H, W] in `dtype`."""
     m = m if dtype == np.float32 else m.astype(dtype)
-    D = m.D
-    x = np.asarray(x, dtype=dtype)
-    s = conditioning(m, t, dtype)
-    h = linear(patchify(x, m.p), m.top["W_pe"], m.top["b_pe"]) + m.top["pos"]
-    for b in m.blocks:
-        mod = linear(s, b["W_mod"], b["b_mod"]).reshape(6, D)
-        shift1, scale1, gate1, shift2, scale2, gate2 = mod
-        a = layer_norm(h) * (1.0 + scale1) + shift1
-        qkv = linear(a, b["W_qkv"], b["b_qkv"])
-        o = attention(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], m.heads)
-        h = h + gate1 * linear(o, b["W_o"], b["b_o"])
-        if m.has_cross:
-            if ctx is None:
-                raise ValueError("network has cross-attention: ctx is required")
-            qx = linear(layer_norm(h), b["W_qx"], b["b_qx"])
-            kv = linear(np.asarray(ctx, dtype=dtype), b["W_kvx"], b["b_kvx"])
-            ox = attention(qx, kv[:, :D], kv[:, D:], m.heads)
-            h = h + linear(ox, b["W_ox"], b["b_ox"])
-        a = layer_norm(h) * (1.0 + scale2) + shift2
-        f = gelu_tanh(linear(a, b["W_fc1"], b["b_fc1"]))
-        h = h + gate2 * linear(f, b["W_fc2"], b["b_fc2"])
-    shift, scale = linear(s, m.top["W_fmod"], m.top["b_fmod"]).reshape(2, D)
+    h, s = residual_one(m, x, t, ctx, None, dtype)
+    shift, scale = linear(s, m.top["W_fmod"], m.top["b_fmod"]).reshape(2, m.D)
     out = linear(layer_norm(h) * (1.0 + scale) + shift, m.top["W_f"], m.top["b_f"])
     return unpatchify(out, m.C, m.H, m.W, m.p)
 
