@@ -1,0 +1,196 @@
+/*
+ * streamflow.h - C ABI of the stream-batched rectified-flow step on MI355X (gfx950).
+ *
+ * The method (StreamFlow, arXiv 2511.22009) keeps a queue of in-flight latents,
+ * each at its own denoising time, and advances all of them with ONE velocity-network
+ * call per step (Sec. 3.2, Eq. 5), followed by a per-sample Euler update
+ * x' = x + (t_next - t) v (Sec. 3.1.1 discretization; Alg. 1, its final update) and a
+ * shift of the queue: fresh noise enters at slot 0 and the oldest latent leaves
+ * finished (Sec. 3.4.1-3.4.2; Alg. 2).
+ *
+ * The velocity network is a DiT-style adaLN transformer that outputs v directly; its
+ * shape comes from the weight blob. Every computation step runs in HIP kernels on the
+ * GPU; the host side only validates arguments and enqueues launches.
+ *
+ * Conventions shared by every call:
+ *   - Latents x, velocities v, z_new and x_done are DEVICE pointers to fp32 NCHW data,
+ *     one latent = C*H*W floats, slots contiguous: x[B][C][H][W].
+ *   - t[] and dt[] are HOST arrays of B floats. They are copied into kernel arguments
+ *     at call time and not retained.
+ *   - Slot 0 is the newest latent (largest t), slot B-1 the oldest (Alg. 2's order:
+ *     the batch is [z_new, buffer] and the finished sample is the last entry).
+ *   - Calls enqueue work on `hip_stream` (a hipStream_t; NULL = the default stream) and
+ *     return without waiting. One handle is used by one host thread at a time.
+ *   - Every call returns SF_OK (0) or a negative SF_E_* code. All argument and blob
+ *     validation happens on the host before any HIP call, so a rejected call has no
+ *     effect. A HIP failure (allocation, launch, or an earlier asynchronous fault seen
+ *     by the launch check) returns SF_E_HIP. Nothing aborts the process.
+ *   - The caller owns every device buffer it passes; the library never frees or keeps
+ *     them. The library owns the weights and workspace inside the handle.
+ */
+#ifndef STREAMFLOW_H
+#define STREAMFLOW_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sf_model sf_model;
+
+/* Status codes. */
+enum {
+  SF_OK = 0,
+  SF_E_INVAL = -1,        /* bad argument (null pointer, size out of range, non-finite t/dt) */
+  SF_E_BLOB = -2,         /* weight blob malformed (magic, version, shape fields, byte count) */
+  SF_E_NOTLOADED = -3,    /* handle is NULL where a loaded model is required */
+  SF_E_OOM = -4,          /* device allocation failed */
+  SF_E_HIP = -5,          /* a HIP runtime call or kernel launch failed */
+  SF_E_UNSUPPORTED = -6   /* valid blob, but a shape this build has no kernel for */
+};
+
+/* Arithmetic modes. BF16: bf16 weights and GEMM/attention operands with fp32
+ * accumulation, fp32 residual stream, latents and velocities. FP32: fp32 throughout. */
+enum { SF_PREC_BF16 = 0, SF_PREC_FP32 = 1 };
+
+/* Largest number of network rows one call may run (latents, doubled under guidance). */
+#define SF_MAX_ROWS 64
+
+/* Conditioning for networks with cross-attention (the conditioning c of Alg. 2's
+ * network call, and its ApplyCFG / HandleCFG steps).
+ *   ctx      device fp32 [B][ctx_len][ctx_dim]: the context of each slot's latent.
+ *   null_ctx device fp32 [ctx_len][ctx_dim]: the unconditional context shared by every
+ *            unconditional row, or NULL for no guidance.
+ *   guidance w: with null_ctx set, the network runs 2B rows (B with ctx, then B with
+ *            null_ctx, each at its slot's t) and v = v_u + w (v_c - v_u). */
+typedef struct sf_cond {
+  const float* ctx;
+  const float* null_ctx;
+  float guidance;
+} sf_cond;
+
+/* Shape and mode of a loaded model. */
+typedef struct sf_info {
+  int C, H, W, p, D, L, heads, mlp, tdim, ctx_len, ctx_dim, has_cross;
+  int tokens;            /* N = (H/p) * (W/p) tokens per latent */
+  int mod_width;         /* L*6*D + 2*D: width of one row of the adaLN table */
+  int precision;         /* SF_PREC_* */
+  int max_rows;
+  size_t weight_bytes;   /* device bytes held for weights */
+  size_t workspace_bytes;/* device bytes held for activations */
+} sf_info;
+
+/* Parse a weight blob, upload the weights (converted to bf16 in SF_PREC_BF16 mode) and
+ * size the workspace for up to `max_rows` network rows (1..SF_MAX_ROWS).
+ *
+ * Blob layout (little-endian): 64-byte header = magic "SFW1", u32 version (1), u32
+ * C,H,W,p,D,L,heads,mlp,tdim,ctx_len,ctx_dim,has_cross, u64 seed; then fp32 tensors:
+ * W_pe[D][p*p*C], b_pe[D], pos[N][D], W_t1[D][tdim], b_t1[D], W_t2[D][D], b_t2[D];
+ * per block W_mod[6D][D], b_mod[6D], W_qkv[3D][D], b_qkv[3D], W_o[D][D], b_o[D],
+ * (if has_cross) W_qx[D][D], b_qx[D], W_kvx[2D][ctx_dim], b_kvx[2D], W_ox[D][D],
+ * b_ox[D], then W_fc1[mlp][D], b_fc1[mlp], W_fc2[D][mlp], b_fc2[D]; finally
+ * W_fmod[2D][D], b_fmod[2D], W_f[p*p*C][D], b_f[p*p*C]. Linear weights are [out][in].
+ * The byte count must match exactly.
+ *
+ * `blob` is a HOST pointer; it is read during the call and not retained. On success
+ * *out owns device memory until sf_free. Errors: SF_E_INVAL (null blob/out, bad
+ * precision or max_rows), SF_E_BLOB, SF_E_UNSUPPORTED (head dim not a multiple of 8
+ * or above 128, a width not a multiple of 8, H or W not a multiple of p), SF_E_OOM,
+ * SF_E_HIP. The environment variable SF_FAIL_ALLOC_AFTER=n makes the (n+1)-th device
+ * allocation of a load fail, to exercise the SF_E_OOM path. */
+int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows, sf_model** out);
+
+/* Release everything the handle owns. NULL is a no-op. Waits for the device. */
+void sf_free(sf_model* m);
+
+/* Text for a status code (static storage). */
+const char* sf_strerror(int code);
+
+/* Copy the model's shape and mode into *info. */
+int sf_get_info(const sf_model* m, sf_info* info);
+
+/* The heterogeneous-timestep network call (Sec. 3.2, Eq. 5): v[k] = v_theta(x[k], t[k])
+ * for k < B, every slot at its own t. x: device [B][C][H][W]; t: host [B] in [0, 1]
+ * (the network sees 1000 t); v: device [B][C][H][W] output. cond: NULL for an
+ * unconditioned network; required when the network has cross-attention (see sf_cond).
+ * Rows run = B, or 2B with guidance; must be <= max_rows. */
+int sf_velocity(sf_model* m, const float* x, const float* t, int B, const sf_cond* cond,
+                float* v, void* hip_stream);
+
+/* One stream step (Eq. 5 network call, then Alg. 1's per-sample Euler update, then
+ * Alg. 2's shift), in place on x:
+ *   v = v_theta(x[0:B], t[0:B]);  x'_k = x_k + dt_k v_k   (dt signed: t_next - t)
+ *   x_done != NULL (full pipeline): x_done <- x'_{B-1}; x[k+1] <- x'_k for k < B-1;
+ *                                   x[0] <- z_new. The queue keeps B slots.
+ *   x_done == NULL (filling):       x[k+1] <- x'_k for k < B; x[0] <- z_new. The queue
+ *                                   grows to B+1 slots, so x must hold B+1 latents.
+ * z_new (device, one latent) is required. The Euler product and sum are rounded
+ * separately (no fused multiply-add), the same as a plain fp32 x + dt * v. */
+int sf_stream_step(sf_model* m, float* x, const float* t, const float* dt, int B,
+                   const sf_cond* cond, const float* z_new, float* x_done, void* hip_stream);
+
+/* The Euler update and shift of sf_stream_step alone, on a caller-supplied velocity
+ * v: device [B][C][H][W]. Same in-place semantics and rounding. */
+int sf_euler_shift(sf_model* m, float* x, const float* v, const float* dt, int B,
+                   const float* z_new, float* x_done, void* hip_stream);
+
+/* The per-sample timestep conditioning alone: for each k < B, the sinusoidal embedding
+ * of 1000 t[k], the timestep MLP, and every adaLN projection. table: device fp32
+ * [B][mod_width]; row k holds, for each block, (shift1, scale1, gate1, shift2, scale2,
+ * gate2) of width D each, then the final layer's (shift, scale). */
+int sf_modulation(sf_model* m, const float* t, int B, float* table, void* hip_stream);
+
+/* Test hook: run the network on B rows (cond as in sf_velocity) through the patch
+ * embedding and the first `blocks` blocks (0..L) and copy the fp32 residual stream to
+ * h: device [rows][N][D]. */
+int sf_residual(sf_model* m, const float* x, const float* t, int B, const sf_cond* cond,
+                int blocks, float* h, void* hip_stream);
+
+/* Internal buffers readable through sf_debug_read. After a network call (sf_velocity,
+ * sf_stream_step or sf_residual) they hold what that call left, i.e. the intermediates
+ * of the LAST block it ran. Element type: fp32 for SF_BUF_H and SF_BUF_TABLE; the
+ * compute type (bf16 in SF_PREC_BF16 mode, else fp32) for the others.
+ *   SF_BUF_H     [rows][N][D]           residual stream
+ *   SF_BUF_ACT   [rows][N][D]           last LayerNorm + modulate output (the MLP input)
+ *   SF_BUF_Q/K   [rows][heads][N][dh]   self-attention queries / keys
+ *   SF_BUF_VT    [rows][heads][dh][ldv] self-attention values, transposed; ldv = N
+ *                                       rounded up to a multiple of 8
+ *   SF_BUF_ATTN  [rows][N][D]           attention output before the output projection
+ *   SF_BUF_MLP   [rows][N][mlp]         GELU(fc1) output
+ *   SF_BUF_TABLE [B][mod_width]         adaLN table (rows k < B) */
+enum { SF_BUF_H = 0, SF_BUF_ACT, SF_BUF_Q, SF_BUF_K, SF_BUF_VT, SF_BUF_ATTN, SF_BUF_MLP, SF_BUF_TABLE };
+
+/* Test hook: copy the first `bytes` bytes of internal buffer `buffer` to device memory
+ * `dst` (enqueued on hip_stream). SF_E_INVAL if bytes exceeds the buffer. */
+int sf_debug_read(sf_model* m, int buffer, void* dst, size_t bytes, void* hip_stream);
+
+/* Kernel classes for event timing. */
+enum {
+  SF_KC_TEMB = 0,   /* timestep embedding, MLP and adaLN projections */
+  SF_KC_EMBED,      /* patchify + patch embed + position table */
+  SF_KC_LN,         /* LayerNorm + adaLN modulate */
+  SF_KC_QKV,        /* QKV projection GEMM */
+  SF_KC_ATTN,       /* self-attention */
+  SF_KC_PROJ,       /* attention output projection GEMM + gated residual */
+  SF_KC_FC1,        /* MLP up-projection GEMM + GELU */
+  SF_KC_FC2,        /* MLP down-projection GEMM + gated residual */
+  SF_KC_CROSS,      /* every cross-attention kernel */
+  SF_KC_HEAD,       /* final LayerNorm + modulate + linear + unpatchify */
+  SF_KC_EULER,      /* guidance combine, Euler update and queue shift */
+  SF_KC_COUNT
+};
+
+/* Test and bench hook: while enabled, every launch of kernel class `kc` is bracketed
+ * by a pair of HIP events recorded on the launch stream (at most 16384 launches are
+ * recorded; later ones are counted but not timed). sf_timing_read waits for the
+ * recorded events, returns the summed milliseconds and the number of timed launches,
+ * and clears the record. */
+int sf_timing_enable(sf_model* m, int kc, int enable);
+int sf_timing_read(sf_model* m, int kc, double* total_ms, long* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STREAMFLOW_H */

@@ -1,0 +1,50 @@
+// Device-side helpers shared by the gfx950 kernels: vector types for the MFMA
+// builtins, wavefront (64-lane) reductions, invariant-divisor division, bf16 I/O.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sf_launch.h"
+
+namespace sf {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// n / d for a divisor fixed at launch: q = (umulhi(n, magic) + n) >> shift.
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
+  return (uint32_t)(((uint64_t)__umulhi(n, f.magic) + n) >> f.shift);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }  // RNE
+
+template <typename T> __device__ __forceinline__ float to_f32(T v) { return (float)v; }
+
+// tanh-form GELU written as z * sigmoid(2u), u = sqrt(2/pi) (z + 0.044715 z^3),
+// since 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)).
+__device__ __forceinline__ float gelu_tanh(float z) {
+  const float k2 = 2.0f * 0.7978845608028654f;  // 2 sqrt(2/pi)
+  float u2 = k2 * (z + 0.044715f * z * z * z);
+  return z / (1.0f + __expf(-u2));
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+}  // namespace sf

@@ -1,0 +1,148 @@
+// Internal interface between the C-ABI runtime (streamflow.cpp) and the gfx950
+// kernels: argument structs and launchers. Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sf {
+
+constexpr int kMaxRows = 64;     // equals SF_MAX_ROWS
+constexpr int kMaxWidth = 2048;  // largest D / mlp input width a row kernel holds
+constexpr int kMaxPatch = 32;    // largest p*p*C
+
+// Per-row scalars passed by value in the kernel argument block (t or dt of each slot).
+struct RowScalars {
+  float v[kMaxRows];
+};
+
+// Division by a divisor fixed for a launch: q = (umulhi(n, magic) + n) >> shift,
+// exact for every 32-bit n (magic from the round-up method for invariant divisors).
+struct FastDiv {
+  uint32_t magic;
+  uint32_t shift;
+  uint32_t d;
+};
+FastDiv make_fastdiv(uint32_t d);
+
+// ---- K1: batched GEMV  Y[b][j] = act(W[j,:] . X[b,:] + bias[j]) ------------------
+// x_mode 1 builds X on the fly as the sinusoidal embedding of 1000 t[b] (width K,
+// [cos | sin] over K/2 frequencies `freqs`).
+struct GemvArgs {
+  const void* W;        // [R][K], bf16 or fp32
+  const float* bias;    // [R]
+  const float* X;       // [B][ldx] (x_mode 0)
+  int ldx;
+  int B, K, R;
+  float* Y;             // [B][ldy]
+  int ldy;
+  int act;              // 0 identity, 1 SiLU
+  int x_mode;           // 0 memory, 1 sinusoid of 1000 t
+  const float* freqs;   // [K/2] (x_mode 1)
+  RowScalars t;         // (x_mode 1)
+};
+hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s);
+
+// ---- K2: patchify + patch embed + position table ---------------------------------
+struct EmbedArgs {
+  const float* x;       // [n_lat][C][H][W]
+  int n_lat;            // network row r reads latent r % n_lat
+  const float* W_pe;    // [D][P]
+  const float* b_pe;    // [D]
+  const float* pos;     // [N][D]
+  float* h;             // [rows*N][D]
+  int rows, C, H, W, p, D, N;
+};
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+
+// Build the context matrix of the cross-attention K/V projection:
+// out[r][l][c] = (r < n_cond ? ctx[r] : null_ctx)[l][c], converted to the compute type.
+hipError_t launch_ctx_assemble(bool use_bf16, const float* ctx, const float* null_ctx, int n_cond,
+                               int rows, int ctx_len, int ctx_dim, void* out, hipStream_t s);
+
+// ---- K5: LayerNorm (+ per-sample adaLN modulate) ---------------------------------
+struct LnArgs {
+  const float* h;       // [M][D] fp32 residual stream
+  void* out;            // [M][D] bf16 or fp32
+  int M, D;
+  const float* table;   // adaLN table [n_slots][ldt], or nullptr for plain LN
+  int ldt, shift_off, scale_off;
+  FastDiv tok;          // divides a token row index by N -> network row
+  int n_slots;          // network row r uses table row (r < n_slots ? r : r - n_slots)
+};
+hipError_t launch_ln(bool out_bf16, const LnArgs& a, hipStream_t s);
+
+// ---- K7: final LN + modulate + linear D -> p*p*C + unpatchify ----------------------
+struct HeadArgs {
+  const float* h;       // [rows*N][D]
+  const float* W_f;     // [P][D]
+  const float* b_f;     // [P]
+  const float* table;
+  int ldt, shift_off, scale_off;
+  int n_slots;
+  FastDiv tok;
+  float* v;             // [rows][C][H][W]
+  int rows, C, H, W, p, D, N, P;
+};
+hipError_t launch_head(const HeadArgs& a, hipStream_t s);
+
+// ---- K3: GEMM  C[M][N] = A[M][K] . B[N][K]^T with a fused epilogue -----------------
+enum EpiKind {
+  EPI_QKV = 0,       // + bias, scatter to head-major q / k and transposed v
+  EPI_RES_GATE = 1,  // h += gate[slot][n] * (acc + bias)
+  EPI_GELU = 2,      // out = GELU_tanh(acc + bias)
+  EPI_RES = 3        // h += acc + bias
+};
+struct GemmArgs {
+  const void* A;
+  int lda;
+  const void* B;
+  int ldb;
+  int M, N, K;
+  const float* bias;
+  // EPI_QKV: column n of the projection is part (which_base + n / D) of {q, k, v},
+  // head (n % D) / dh, dim (n % D) % dh; row m is token m % ntok of network row m / ntok.
+  void* q;
+  void* k;
+  void* vT;             // [rows][heads][dh][ldv]
+  int heads, dh, D, ntok, ldv, which_base;
+  FastDiv div_ntok, div_D, div_dh;
+  // EPI_RES_GATE / EPI_RES
+  float* h;
+  int ldh;
+  const float* table;
+  int ldt, gate_off, n_slots;
+  // EPI_GELU
+  void* out;
+  int ldo;
+};
+hipError_t launch_gemm(bool use_bf16, EpiKind kind, const GemmArgs& a, hipStream_t s);
+
+// ---- K4: softmax attention per (network row, head) ---------------------------------
+struct AttnArgs {
+  const void* q;        // [rows][heads][Nq][dh]
+  const void* k;        // [rows][heads][Nk][dh]
+  const void* vT;       // [rows][heads][dh][ldv], columns >= Nk are zero
+  void* o;              // [rows][Nq][D], head j at columns j*dh ..
+  int rows, heads, Nq, Nk, dh, ldv, D;
+  float scale;          // 1 / sqrt(dh)
+};
+hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s);
+bool attention_supports(int dh);
+
+// ---- K6: guidance combine + Euler update + queue shift -----------------------------
+struct EulerArgs {
+  float* x;             // [B(+1)][E] slots, updated in place
+  const float* v;       // [B][E], or [2B][E] (cond rows then uncond rows) with guidance
+  int B, E;
+  int guided;
+  float w;
+  RowScalars dt;
+  const float* z_new;   // [E]
+  float* x_done;        // [E] or nullptr (filling: the queue grows to B+1)
+};
+hipError_t launch_euler_shift(const EulerArgs& a, hipStream_t s);
+// v_out[k] = v[B+k] + w (v[k] - v[B+k]) for k < B.
+hipError_t launch_cfg_combine(const float* v, int B, int E, float w, float* v_out, hipStream_t s);
+
+}  // namespace sf

@@ -1,0 +1,69 @@
+"""Per-kernel parity on the GPU: each kernel's output against the oracle applied to the
+SAME inputs the kernel saw (read back from the library's workspace), so an error is
+pinned to one kernel instead of the whole network."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from conftest import oracle_model
+from helpers import rel_l2
+
+pytestmark = pytest.mark.gpu
+
+from gpu_util import dev, host, model, torch  # noqa: E402
+from paper_2511_22009_amd import Buffer  # noqa: E402
+
+# tolerance of a kernel fed exactly its own inputs: fp32 arithmetic, or a bf16 output
+ISO = {"fp32": 1e-5, "bf16": 1e-2}
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+
+
+def _run_block0(name, prec):
+    cfg = W.get_config(name)
+    t, _ = W.slot_times(cfg)
+    x = W.latents(cfg, cfg.K)
+    m = model(name, prec)
+    R, N, D, H, dh = cfg.K, cfg.N, cfg.D, cfg.heads, cfg.dh
+    h1 = host(m.residual(dev(x), t, 1))
+    ldv = (N + 7) // 8 * 8
+    bufs = dict(
+        q=host(m.debug_read(Buffer.Q, (R, H, N, dh))).transpose(0, 2, 1, 3).reshape(R, N, D),
+        k=host(m.debug_read(Buffer.K, (R, H, N, dh))).transpose(0, 2, 1, 3).reshape(R, N, D),
+        v=host(m.debug_read(Buffer.VT, (R, H, dh, ldv)))[..., :N].transpose(0, 3, 1, 2).reshape(R, N, D),
+        attn=host(m.debug_read(Buffer.ATTN, (R, N, D))),
+        ln2=host(m.debug_read(Buffer.ACT, (R, N, D))),
+        mlp=host(m.debug_read(Buffer.MLP, (R, N, cfg.mlp))),
+        h_out=h1,
+    )
+    om = oracle_model(name)
+    traces = []
+    for k in range(R):
+        tr = {}
+        oracle.residual_one(om, x[k], t[k], None, 1, trace=tr)
+        traces.append(tr)
+    return cfg, om, bufs, traces
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+@pytest.mark.parametrize("name", ["tiny_tsens", "ragged", "dh72"])
+def test_block0_intermediates(name, prec):
+    cfg, om, g, tr = _run_block0(name, prec)
+    b = om.blocks[0]
+    report = {}
+    for k in range(cfg.K):
+        # end-to-end intermediates vs the oracle's own chain
+        for key in ("q", "k", "v", "attn", "ln2", "mlp", "h_out"):
+            report.setdefault(key, []).append(rel_l2(g[key][k], tr[k][key]))
+        # each kernel on its own inputs
+        a_iso = oracle.attention(g["q"][k].astype(np.float64), g["k"][k].astype(np.float64),
+                                 g["v"][k].astype(np.float64), cfg.heads)
+        report.setdefault("attn_iso", []).append(rel_l2(g["attn"][k], a_iso))
+        f_iso = oracle.gelu_tanh(g["ln2"][k].astype(np.float64) @ b["W_fc1"].T.astype(np.float64) + b["b_fc1"])
+        report.setdefault("fc1_iso", []).append(rel_l2(g["mlp"][k], f_iso))
+    worst = {k: max(v) for k, v in report.items()}
+    print(name, prec, {k: f"{v:.2e}" for k, v in worst.items()})
+    assert worst["attn_iso"] <= ISO[prec], worst
+    assert worst["fc1_iso"] <= ISO[prec], worst
+    for key in ("q", "k", "v", "attn", "ln2", "mlp", "h_out"):
+        assert worst[key] <= TOL[prec], worst
