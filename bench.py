@@ -1,0 +1,209 @@
+"""Benchmark: stream-batched rectified-flow steps on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config s512] [--no-cpu]
+
+A step is one sf_stream_step over a full queue: one heterogeneous-timestep velocity
+network call over every in-flight latent, each latent's Euler update, and the shift
+that admits the next fresh latent (one finished latent leaves per step). Inputs
+(weights, latents, a pool of fresh latents) are resident in HBM before timing.
+
+Prints one JSON line: latent-steps/s (value), images/s, the roofline of the dominant
+kernel class (timed with HIP events on the launch stream during the timed steps),
+the per-class time breakdown, the one-latent-at-a-time rate (no stream batching),
+and the oracle timed on the host cores as a CPU baseline.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+METRIC = "stream-batched RF latent-steps/s and images/s at 512² (K=4); MFMA util %"
+MI355X_PEAK_BF16_TFLOPS = 2500.0
+MI355X_PEAK_FP32_TFLOPS = 157.3
+MI355X_HBM_GBS = 8000.0
+
+
+def class_work(cfg, kc, rows):
+    """Algorithmic FLOPs of ONE launch of kernel class kc (GEMM classes and attention)."""
+    from paper_2511_22009_amd import KernelClass as KC
+    M, D, N, F = rows * cfg.N, cfg.D, cfg.N, cfg.mlp
+    return {
+        KC.QKV: 2.0 * M * D * 3 * D,
+        KC.PROJ: 2.0 * M * D * D,
+        KC.FC1: 2.0 * M * D * F,
+        KC.FC2: 2.0 * M * F * D,
+        KC.ATTN: 4.0 * rows * N * N * D,
+    }.get(kc)
+
+
+def cpu_baseline(cfg, budget_s=12.0):
+    """Oracle stream steps on the host cores until about budget_s seconds of work."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    blob = W.make_blob(cfg)
+    m = oracle.load_blob(blob)
+    t, dt = W.slot_times(cfg)
+    x = W.latents(cfg, cfg.K)
+    kw = {}
+    if cfg.cfg:
+        kw = dict(ctx=W.context(cfg, cfg.K), null_ctx=W.null_context(cfg), guidance=cfg.guidance)
+    # one sample's forward first, to size the run
+    t0 = time.perf_counter()
+    oracle.stream_step(m, x[:1], t[:1], dt[:1], x[0], **({k: (v[:1] if k == "ctx" else v) for k, v in kw.items()}))
+    one = time.perf_counter() - t0
+    steps = max(1, int(budget_s / max(one * cfg.K, 1e-9)))
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        x, _, _ = oracle.stream_step(m, x, t, dt, x[0], **kw)
+    el = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    return {"value": cfg.K * steps / el, "unit": "latent-steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{steps} full stream step(s) of the {cfg.name} workload ({cfg.K} latents each), "
+                      f"NumPy fp32, {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="s512")
+    ap.add_argument("--precision", default="bf16", choices=["bf16", "fp32"])
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested): the stream step has no "
+              "multi-GPU path; independent queues per GPU would each report this single-GPU rate.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2511_22009_amd import Cond, KernelClass, Model, Precision
+
+    cfg = W.get_config(args.config)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    blob = W.make_blob(cfg)
+    m = Model(blob, Precision[args.precision.upper()], max_rows=cfg.rows)
+    t, dt = W.slot_times(cfg)
+    K = cfg.K
+    x = torch.from_numpy(W.latents(cfg, K)).to(dev)
+    pool = torch.from_numpy(W.latents(cfg, 16, seed=W.gen.SEED_IMAGE_BASE)).to(dev)
+    done = torch.empty(cfg.latent_shape, device=dev)
+    cond = None
+    if cfg.has_cross:
+        cond = Cond(torch.from_numpy(W.context(cfg, K)).to(dev), torch.from_numpy(W.null_context(cfg)).to(dev),
+                    cfg.guidance)
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        m.stream_step(x, t, dt, K, pool[i % pool.shape[0]], done, cond, stream)
+
+    # warmup, with every kernel class timed to find the dominant one
+    for kc in KernelClass:
+        m.timing_enable(kc, True)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    breakdown = {}
+    for kc in KernelClass:
+        ms, n = m.timing_read(kc)
+        m.timing_enable(kc, False)
+        if n:
+            breakdown[kc.name] = {"ms_per_step": ms / max(args.warmup, 1), "launches_per_step": n / max(args.warmup, 1)}
+    dom = max((kc for kc in KernelClass if kc.name in breakdown and class_work(cfg, kc, cfg.rows)),
+              key=lambda kc: breakdown[kc.name]["ms_per_step"])
+
+    # timed region: exactly `steps` steps, events on the dominant class only
+    m.timing_enable(dom, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    dom_ms, dom_n = m.timing_read(dom)
+    m.timing_enable(dom, False)
+    if not bool(torch.isfinite(x).all()):
+        raise RuntimeError("non-finite latents after the timed steps")
+
+    ms_step = 1e3 * el / args.steps
+    value = K / (el / args.steps)
+    work = class_work(cfg, dom, cfg.rows)
+    avg_launch_s = dom_ms / 1e3 / max(dom_n, 1)
+    achieved = work / avg_launch_s / 1e12
+    peak = MI355X_PEAK_BF16_TFLOPS if args.precision == "bf16" else MI355X_PEAK_FP32_TFLOPS
+    gemm_ms = sum(breakdown[k]["ms_per_step"] for k in ("QKV", "PROJ", "FC1", "FC2") if k in breakdown)
+    gemm_tflops = cfg.gemm_flops_per_step() / (gemm_ms / 1e3) / 1e12 if gemm_ms else None
+
+    # the same kernels one latent at a time (no stream batching): K network calls per image
+    seq_steps = max(4, args.steps // 10)
+    x1 = x[:1].clone()
+    done1 = torch.empty_like(done)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    cond1 = None if cond is None else Cond(cond.ctx[:1], cond.null_ctx, cond.guidance)
+    for i in range(seq_steps):
+        for s in range(K):
+            # a one-slot queue: the updated latent leaves through `done1` and, until the
+            # image is finished, re-enters slot 0 as the "fresh" latent
+            z = done1 if s < K - 1 else pool[i % pool.shape[0]]
+            m.stream_step(x1, t[s:s + 1], dt[s:s + 1], 1, z, done1, cond1, stream)
+    torch.cuda.synchronize()
+    seq_img_s = seq_steps / (time.perf_counter() - t1)
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "latent-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.precision,
+        "data": "synthetic (seeded random-init weights N(0,0.02), N(0,1) latents)",
+        "config": {
+            "workload": f"{cfg.name}: latent {cfg.C}x{cfg.H}x{cfg.W}, {cfg.N} tokens, width {cfg.D}, depth {cfg.L}, "
+                        f"{cfg.heads} heads, MLP {cfg.mlp}, {K} stream slots ({cfg.rows} network rows), "
+                        f"schedule {cfg.schedule}",
+            "slots": K, "rows": cfg.rows, "tokens": cfg.N, "width": cfg.D, "depth": cfg.L,
+        },
+        "images_per_s": 1e3 / ms_step,
+        "step_tflops": cfg.flops_per_step() / (ms_step / 1e3) / 1e12,
+        "step_frac_of_peak": cfg.flops_per_step() / (ms_step / 1e3) / 1e12 / peak,
+        "gemm_tflops": gemm_tflops,
+        "gemm_frac_of_peak": (gemm_tflops / peak) if gemm_tflops else None,
+        "sequential_images_per_s": seq_img_s,
+        "roofline": {
+            "kernel": dom.name,
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": achieved / peak,
+            "traffic": None,
+            "flops_per_launch": work,
+            "avg_launch_us": avg_launch_s * 1e6,
+            "launches_timed": dom_n,
+        },
+        "breakdown_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in breakdown.items()},
+    }
+    m.close()
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(cfg)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -47,4 +47,15 @@ __device__ __forceinline__ float gelu_tanh(float z) {
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
+// Raw buffer resource over [base, base + bytes): a load whose byte offset is at or
+// past `bytes` returns zeros in hardware, so tile loads need no branches.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kOffOOB = 0x7ffffff0;  // any offset >= every buffer size used here
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
 }  // namespace sf
