@@ -216,3 +216,51 @@ def _euler_gpu(m, x, v, dt):
     done = torch.empty(tuple(x.shape[1:]), device="cuda")
     m.euler_shift(buf, v, np.float32([dt]), 1, x[0], done)
     return done[None]
+
+
+# ------------------------------------------------- cross-attention and guidance
+
+def _cfg_inputs():
+    cfg = W.get_config("tiny_cfg")
+    t, dt = W.slot_times(cfg)
+    return cfg, W.latents(cfg, cfg.K), t, dt, W.context(cfg, cfg.K), W.null_context(cfg)
+
+
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("guided", [True, False], ids=["guided", "cond_only"])
+def test_cross_attention_velocity_parity(prec, guided):
+    from paper_2511_22009_amd import Cond
+    cfg, x, t, _, ctx, nctx = _cfg_inputs()
+    m = model("tiny_cfg", prec)
+    w = cfg.guidance if guided else None
+    ref = oracle.velocity(oracle_model("tiny_cfg"), x, t, ctx, nctx if guided else None, w)
+    cond = Cond(dev(ctx), dev(nctx) if guided else None, cfg.guidance)
+    got = host(m.velocity(dev(x), t, cond))
+    errs = [rel_l2(got[k], ref[k]) for k in range(cfg.K)]
+    assert max(errs) <= TOL[prec], errs
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_guided_stream_step_parity(prec):
+    from paper_2511_22009_amd import Cond
+    cfg, x, t, dt, ctx, nctx = _cfg_inputs()
+    z = W.z_new_for_image(cfg, 3)
+    _, _, v_ref = oracle.stream_step(oracle_model("tiny_cfg"), x, t, dt, z, True, ctx, nctx, cfg.guidance)
+    xd = dev(x)
+    done = torch.empty(cfg.latent_shape, device="cuda")
+    model("tiny_cfg", prec).stream_step(xd, t, dt, cfg.K, dev(z), done, Cond(dev(ctx), dev(nctx), cfg.guidance))
+    got = host(xd)
+    new = np.concatenate([got[1:], host(done)[None]])
+    np.testing.assert_array_equal(got[0], z)
+    for k in range(cfg.K):
+        assert rel_l2(new[k] - x[k], dt[k] * v_ref[k]) <= TOL[prec]
+
+
+def test_guidance_weight_zero_gives_unconditional_rows():
+    """w = 0 must return exactly the unconditional rows (v_u + 0 (v_c - v_u) = v_u)."""
+    from paper_2511_22009_amd import Cond
+    cfg, x, t, _, ctx, nctx = _cfg_inputs()
+    m = model("tiny_cfg", "fp32")
+    v0 = host(m.velocity(dev(x), t, Cond(dev(ctx), dev(nctx), 0.0)))
+    vu = host(m.velocity(dev(x), t, Cond(dev(np.repeat(nctx[None], cfg.K, 0)), None, 0.0)))
+    np.testing.assert_array_equal(v0, vu)
