@@ -107,10 +107,15 @@ def main():
     def step(i):
         m.stream_step(x, t, dt, K, pool[i % pool.shape[0]], done, cond, stream)
 
-    # warmup, with every kernel class timed to find the dominant one
+    # warmup (untimed), then a separate pass with every kernel class event-timed to
+    # get the per-class breakdown and pick the dominant class
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    n_break = max(3, min(10, args.steps))
     for kc in KernelClass:
         m.timing_enable(kc, True)
-    for i in range(args.warmup):
+    for i in range(n_break):
         step(i)
     torch.cuda.synchronize()
     breakdown = {}
@@ -118,7 +123,7 @@ def main():
         ms, n = m.timing_read(kc)
         m.timing_enable(kc, False)
         if n:
-            breakdown[kc.name] = {"ms_per_step": ms / max(args.warmup, 1), "launches_per_step": n / max(args.warmup, 1)}
+            breakdown[kc.name] = {"ms_per_step": ms / n_break, "launches_per_step": n / n_break}
     dom = max((kc for kc in KernelClass if kc.name in breakdown and class_work(cfg, kc, cfg.rows)),
               key=lambda kc: breakdown[kc.name]["ms_per_step"])
 

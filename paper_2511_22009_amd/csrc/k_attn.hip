@@ -31,13 +31,23 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, g = lane >> 5;
-  const int head = blockIdx.y, r = blockIdx.z;
+  // Workgroup b runs on XCD b % 8. Give each XCD a contiguous range of (row, head,
+  // query block) triples, query blocks fastest, so the query blocks that stream the same
+  // K and V share one L2.
+  const int nqb = (a.Nq + kQB - 1) / kQB;
+  const int T = nqb * a.heads * a.rows;
+  const int xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  const int base = T / 8, rem = T % 8;
+  const int logical = xcd * base + min(xcd, rem) + local;
+  const int qblk = logical % nqb;
+  const int rh = logical / nqb;
+  const int head = rh % a.heads, r = rh / a.heads;
   const int dh = a.dh;
   const size_t bh = (size_t)r * a.heads + head;
   const bf16* Q = (const bf16*)a.q + bh * a.Nq * dh;
   const bf16* Kg = (const bf16*)a.k + bh * a.Nk * dh;
   const bf16* Vt = (const bf16*)a.vT + bh * dh * a.ldv;
-  const int qi = blockIdx.x * kQB + wave * 32 + l32;
+  const int qi = qblk * kQB + wave * 32 + l32;
 
   // zero both buffers once: padding columns/rows are never written by the staging
   for (int i = tid; i < 2 * kBKV * KLD; i += 256) (&Ks[0][0])[i] = (bf16)0.0f;
@@ -57,43 +67,42 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 
   const int kchunks = kBKV * (dh >> 3);       // K tile: kBKV rows x dh/8 chunks
   const int vchunks = dh * (kBKV / 8);        // V^T tile: dh rows x 8 chunks
-  uint4 rk[KCH], rv[VCH];
+  // K and V^T come in through raw buffer loads: keys past Nk (K) and columns past the
+  // padded row (V^T) get an out-of-range offset and read as zeros, without branches.
+  const __amdgpu_buffer_rsrc_t k_src = buffer_rsrc(Kg, (uint32_t)a.Nk * dh * 2);
+  const __amdgpu_buffer_rsrc_t v_src = buffer_rsrc(Vt, (uint32_t)dh * a.ldv * 2);
+  int k_row[KCH], k_col[KCH], v_off[VCH], v_kv[VCH];
+#pragma unroll
+  for (int i = 0; i < KCH; ++i) {
+    const int c = tid + i * 256;
+    k_row[i] = c < kchunks ? c / (dh >> 3) : 1 << 20;
+    k_col[i] = c < kchunks ? (c - (c / (dh >> 3)) * (dh >> 3)) * 8 : 0;
+  }
+#pragma unroll
+  for (int i = 0; i < VCH; ++i) {
+    const int c = tid + i * 256;
+    v_kv[i] = (c & 7) * 8;
+    v_off[i] = c < vchunks ? ((c >> 3) * a.ldv + v_kv[i]) * 2 : kOffOOB;
+  }
+  u32x4 rk[KCH], rv[VCH];
   auto gload = [&](int kv0) {
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
-      const int c = tid + i * 256;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (c < kchunks) {
-        const int row = c / (dh >> 3), ch = c - row * (dh >> 3);
-        if (kv0 + row < a.Nk) val = *(const uint4*)(Kg + (size_t)(kv0 + row) * dh + ch * 8);
-      }
-      rk[i] = val;
+      const int row = kv0 + k_row[i];
+      rk[i] = buffer_load16(k_src, row < a.Nk ? (row * dh + k_col[i]) * 2 : kOffOOB);
     }
 #pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int c = tid + i * 256;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (c < vchunks) {
-        const int d = c >> 3, ch = c & 7;
-        const int kv = kv0 + ch * 8;
-        if (kv < a.ldv) val = *(const uint4*)(Vt + (size_t)d * a.ldv + kv);
-      }
-      rv[i] = val;
-    }
+    for (int i = 0; i < VCH; ++i)
+      rv[i] = buffer_load16(v_src, (v_off[i] != kOffOOB && kv0 + v_kv[i] < a.ldv) ? v_off[i] + 2 * kv0 : kOffOOB);
   };
   auto lstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + i * 256;
-      if (c < kchunks) {
-        const int row = c / (dh >> 3), ch = c - row * (dh >> 3);
-        *(uint4*)&Ks[buf][row * KLD + ch * 8] = rk[i];
-      }
-    }
+    for (int i = 0; i < KCH; ++i)
+      if (tid + i * 256 < kchunks) *(u32x4*)&Ks[buf][k_row[i] * KLD + k_col[i]] = rk[i];
 #pragma unroll
     for (int i = 0; i < VCH; ++i) {
       const int c = tid + i * 256;
-      if (c < vchunks) *(uint4*)&Vs[buf][(c >> 3) * VLD + (c & 7) * 8] = rv[i];
+      if (c < vchunks) *(u32x4*)&Vs[buf][(c >> 3) * VLD + (c & 7) * 8] = rv[i];
     }
   };
 
@@ -248,7 +257,7 @@ bool attention_supports(int dh) { return dh >= 8 && dh <= 128 && dh % 8 == 0; }
 
 template <int DHC, int DB>
 static void launch_bf16_inst(const AttnArgs& a, hipStream_t s) {
-  dim3 grid((a.Nq + kQB - 1) / kQB, a.heads, a.rows);
+  dim3 grid(((a.Nq + kQB - 1) / kQB) * a.heads * a.rows);
   hipLaunchKernelGGL((attn_bf16_kernel<DHC, DB>), grid, dim3(256), 0, s, a);
 }
 

@@ -10,7 +10,8 @@
 
 namespace sf {
 
-constexpr int kGemvSamples = 8;  // samples staged in LDS per pass
+constexpr int kGemvSamples = 4;  // samples per pass (inputs held in registers)
+constexpr int kGemvRows = 4;     // weight rows a wavefront streams at once
 
 template <typename WT>
 __device__ __forceinline__ void load4(const WT* p, float* w);
@@ -27,73 +28,106 @@ __device__ __forceinline__ void load4<bf16>(const bf16* p, float* w) {
   w[0] = (float)v[0]; w[1] = (float)v[1]; w[2] = (float)v[2]; w[3] = (float)v[3];
 }
 
-// One wavefront per output row j; lanes stride the row four elements at a time and
-// the samples' input vectors sit in LDS.
-template <typename WT>
+// Lane `lane` owns elements 4*(lane + 64 c) .. +3 of the input width for c < NCH, so its
+// slice of every sample's input vector stays in registers for all rows; a wavefront
+// streams kGemvRows weight rows at a time (independent loads in flight) and reduces
+// each row's partial sums across the 64 lanes at the end.
+template <typename WT, int NCH>
 __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
-  extern __shared__ float xs[];  // [kGemvSamples][K]
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int nw = gridDim.x * 4;
   const WT* W = (const WT*)a.W;
   for (int b0 = 0; b0 < a.B; b0 += kGemvSamples) {
     const int nb = min(kGemvSamples, a.B - b0);
-    for (int i = threadIdx.x; i < nb * a.K; i += blockDim.x) {
-      const int bb = i / a.K, k = i - bb * a.K;
-      float val;
-      if (a.x_mode == 1) {
-        const int half = a.K >> 1;
-        const int f = k < half ? k : k - half;
-        const float tau = 1000.0f * a.t.v[b0 + bb];
-        const float phi = tau * a.freqs[f];
-        val = k < half ? cosf(phi) : sinf(phi);
-      } else {
-        val = a.X[(size_t)(b0 + bb) * a.ldx + k];
-      }
-      xs[bb * a.K + k] = val;
-    }
-    __syncthreads();
-    for (int j = blockIdx.x * 4 + wave; j < a.R; j += gridDim.x * 4) {
-      float acc[kGemvSamples];
+    float x[kGemvSamples][NCH][4];
 #pragma unroll
-      for (int bb = 0; bb < kGemvSamples; ++bb) acc[bb] = 0.0f;
-      const WT* wr = W + (size_t)j * a.K;
-      for (int k = lane * 4; k < a.K; k += 256) {
-        float w[4];
-        load4<WT>(wr + k, w);
+    for (int bb = 0; bb < kGemvSamples; ++bb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int k = 4 * (lane + 64 * c) + e;
+          float v = 0.0f;
+          if (bb < nb && k < a.K) {
+            if (a.x_mode == 1) {
+              const int half = a.K >> 1;
+              const int f = k < half ? k : k - half;
+              const float tau = 1000.0f * a.t.v[b0 + bb];
+              const float phi = tau * a.freqs[f];
+              v = k < half ? cosf(phi) : sinf(phi);
+            } else {
+              v = a.X[(size_t)(b0 + bb) * a.ldx + k];
+            }
+          }
+          x[bb][c][e] = v;
+        }
+    for (int j0 = gw * kGemvRows; j0 < a.R; j0 += nw * kGemvRows) {
+      float acc[kGemvRows][kGemvSamples];
+#pragma unroll
+      for (int rr = 0; rr < kGemvRows; ++rr)
+#pragma unroll
+        for (int bb = 0; bb < kGemvSamples; ++bb) acc[rr][bb] = 0.0f;
+#pragma unroll
+      for (int rr = 0; rr < kGemvRows; ++rr) {
+        const int j = min(j0 + rr, a.R - 1);
+        const WT* wr = W + (size_t)j * a.K;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          const int k = 4 * (lane + 64 * c);
+          if (k < a.K) {
+            float w[4];
+            load4<WT>(wr + k, w);
+            // explicit fma chain: every sample slot runs the same operation sequence, so
+            // a sample's result does not depend on which slot of the batch it sits in
+#pragma unroll
+            for (int bb = 0; bb < kGemvSamples; ++bb) {
+              float t = acc[rr][bb];
+              t = fmaf(w[0], x[bb][c][0], t);
+              t = fmaf(w[1], x[bb][c][1], t);
+              t = fmaf(w[2], x[bb][c][2], t);
+              t = fmaf(w[3], x[bb][c][3], t);
+              acc[rr][bb] = t;
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int rr = 0; rr < kGemvRows; ++rr) {
+        const int j = j0 + rr;
 #pragma unroll
         for (int bb = 0; bb < kGemvSamples; ++bb) {
-          if (bb < nb) {
-            const float* xp = xs + bb * a.K + k;
-            acc[bb] += w[0] * xp[0] + w[1] * xp[1] + w[2] * xp[2] + w[3] * xp[3];
-          }
-        }
-      }
-#pragma unroll
-      for (int bb = 0; bb < kGemvSamples; ++bb) {
-        if (bb < nb) {
-          float s = wave_sum(acc[bb]);
-          if (lane == 0) {
-            s += a.bias[j];
-            if (a.act == 1) s = silu(s);
-            a.Y[(size_t)(b0 + bb) * a.ldy + j] = s;
+          if (bb >= nb) continue;
+          float sum = wave_sum(acc[rr][bb]);
+          if (lane == 0 && j < a.R) {
+            sum += a.bias[j];
+            if (a.act == 1) sum = silu(sum);
+            a.Y[(size_t)(b0 + bb) * a.ldy + j] = sum;
           }
         }
       }
     }
-    __syncthreads();
   }
 }
 
-hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s) {
-  const int rows_per_block = 4;
-  int grid = (a.R + rows_per_block - 1) / rows_per_block;
-  if (grid > 2048) grid = 2048;
-  const size_t lds = sizeof(float) * kGemvSamples * a.K;
-  if (w_bf16)
-    hipLaunchKernelGGL(gemv_kernel<bf16>, dim3(grid), dim3(256), lds, s, a);
-  else
-    hipLaunchKernelGGL(gemv_kernel<float>, dim3(grid), dim3(256), lds, s, a);
+template <typename WT>
+static hipError_t launch_gemv_t(const GemvArgs& a, hipStream_t s) {
+  const int nch = (a.K + 255) / 256;
+  int grid = (a.R + 4 * kGemvRows - 1) / (4 * kGemvRows);
+  if (grid > 1024) grid = 1024;
+  switch (nch) {
+#define SF_GEMV_CASE(n) \
+  case n: hipLaunchKernelGGL((gemv_kernel<WT, n>), dim3(grid), dim3(256), 0, s, a); break;
+    SF_GEMV_CASE(1) SF_GEMV_CASE(2) SF_GEMV_CASE(3) SF_GEMV_CASE(4) SF_GEMV_CASE(5)
+    SF_GEMV_CASE(6) SF_GEMV_CASE(7) SF_GEMV_CASE(8)
+#undef SF_GEMV_CASE
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
+}
+
+hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s) {
+  return w_bf16 ? launch_gemv_t<bf16>(a, s) : launch_gemv_t<float>(a, s);
 }
 
 // One workgroup per token: gather the token's p*p*C patch values (feature

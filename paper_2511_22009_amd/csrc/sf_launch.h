@@ -117,6 +117,9 @@ struct GemmArgs {
   int ldo;
 };
 hipError_t launch_gemm(bool use_bf16, EpiKind kind, const GemmArgs& a, hipStream_t s);
+// The same with an explicit bf16 tile shape (index into the tile table; -1 = choose).
+hipError_t launch_gemm_tile(bool use_bf16, int tile, EpiKind kind, const GemmArgs& a, hipStream_t s);
+int choose_gemm_tile(int M, int N, int K);
 
 // ---- K4: softmax attention per (network row, head) ---------------------------------
 struct AttnArgs {
