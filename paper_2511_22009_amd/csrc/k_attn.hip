@@ -135,33 +135,43 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[c], 0, 0, 0);
       }
     }
-    // s[c][e]: query l32, key kv0 + c*32 + (e/4)*8 + g*4 + e%4
-    float tmax = -INFINITY;
+    // s[c][e]: query l32, key kv0 + c*32 + (e/4)*8 + g*4 + e%4. Raw scores; the
+    // scale (log2 e / sqrt(dh)) is folded into the exp2 argument. Only the last,
+    // ragged tile needs the key mask.
+    if (kv0 + kBKV > a.Nk) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int kv = kv0 + c * 32 + (e >> 2) * 8 + g * 4 + (e & 3);
+          if (kv >= a.Nk) s[c][e] = -INFINITY;
+        }
+    }
+    float tmax = s[0][0];
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int kv = kv0 + c * 32 + (e >> 2) * 8 + g * 4 + (e & 3);
-        const float val = kv < a.Nk ? s[c][e] * sl2 : -INFINITY;
-        s[c][e] = val;
-        tmax = fmaxf(tmax, val);
-      }
+      for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, s[c][e]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
     const float mnew = fmaxf(mrow, tmax);
-    const float alpha = exp2f(mrow - mnew);
+    // rescale the running output and sum only when some query's max moved
+    if (__any(mnew != mrow)) {
+      const float alpha = __builtin_amdgcn_exp2f((mrow - mnew) * sl2);
+      lsum *= alpha;
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
+    }
     mrow = mnew;
-    lsum *= alpha;
-#pragma unroll
-    for (int b = 0; b < DB; ++b)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
+    const float moff = -mnew * sl2;
 
     bf16x8 pf[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float p = exp2f(s[ks >> 1][(ks & 1) * 8 + j] - mnew);
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[ks >> 1][(ks & 1) * 8 + j], sl2, moff));
         lsum += p;
         pf[ks][j] = (bf16)p;
       }

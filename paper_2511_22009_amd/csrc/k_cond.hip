@@ -11,7 +11,6 @@
 namespace sf {
 
 constexpr int kGemvSamples = 4;  // samples per pass (inputs held in registers)
-constexpr int kGemvRows = 4;     // weight rows a wavefront streams at once
 
 template <typename WT>
 __device__ __forceinline__ void load4(const WT* p, float* w);
@@ -32,7 +31,7 @@ __device__ __forceinline__ void load4<bf16>(const bf16* p, float* w) {
 // slice of every sample's input vector stays in registers for all rows; a wavefront
 // streams kGemvRows weight rows at a time (independent loads in flight) and reduces
 // each row's partial sums across the 64 lanes at the end.
-template <typename WT, int NCH>
+template <typename WT, int NCH, int kGemvRows>
 __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
   const int lane = threadIdx.x & 63;
   const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -92,32 +91,48 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
           }
         }
       }
+      if constexpr (kGemvRows * kGemvSamples == 16) {
+        float v16[16];
 #pragma unroll
-      for (int rr = 0; rr < kGemvRows; ++rr) {
+        for (int rr = 0; rr < kGemvRows; ++rr)
+#pragma unroll
+          for (int bb = 0; bb < kGemvSamples; ++bb) v16[rr * kGemvSamples + bb] = acc[rr][bb];
+        float sum = wave_reduce16(v16);
+        const int idx = (lane >> 2) & 15;
+        const int rr = idx / kGemvSamples, bb = idx % kGemvSamples;
         const int j = j0 + rr;
-#pragma unroll
-        for (int bb = 0; bb < kGemvSamples; ++bb) {
-          if (bb >= nb) continue;
-          float sum = wave_sum(acc[rr][bb]);
-          if (lane == 0 && j < a.R) {
-            sum += a.bias[j];
-            if (a.act == 1) sum = silu(sum);
-            a.Y[(size_t)(b0 + bb) * a.ldy + j] = sum;
-          }
+        if ((lane & 3) == 0 && bb < nb && j < a.R) {
+          sum += a.bias[j];
+          if (a.act == 1) sum = silu(sum);
+          a.Y[(size_t)(b0 + bb) * a.ldy + j] = sum;
         }
+      } else {
+#pragma unroll
+        for (int rr = 0; rr < kGemvRows; ++rr)
+#pragma unroll
+          for (int bb = 0; bb < kGemvSamples; ++bb) {
+            if (bb >= nb) continue;
+            float sum = wave_sum(acc[rr][bb]);
+            const int j = j0 + rr;
+            if (lane == 0 && j < a.R) {
+              sum += a.bias[j];
+              if (a.act == 1) sum = silu(sum);
+              a.Y[(size_t)(b0 + bb) * a.ldy + j] = sum;
+            }
+          }
       }
     }
   }
 }
 
-template <typename WT>
-static hipError_t launch_gemv_t(const GemvArgs& a, hipStream_t s) {
+template <typename WT, int ROWS>
+static hipError_t launch_gemv_rows(const GemvArgs& a, hipStream_t s) {
   const int nch = (a.K + 255) / 256;
-  int grid = (a.R + 4 * kGemvRows - 1) / (4 * kGemvRows);
-  if (grid > 1024) grid = 1024;
+  int grid = (a.R + 4 * ROWS - 1) / (4 * ROWS);
+  if (grid > 2048) grid = 2048;
   switch (nch) {
 #define SF_GEMV_CASE(n) \
-  case n: hipLaunchKernelGGL((gemv_kernel<WT, n>), dim3(grid), dim3(256), 0, s, a); break;
+  case n: hipLaunchKernelGGL((gemv_kernel<WT, n, ROWS>), dim3(grid), dim3(256), 0, s, a); break;
     SF_GEMV_CASE(1) SF_GEMV_CASE(2) SF_GEMV_CASE(3) SF_GEMV_CASE(4) SF_GEMV_CASE(5)
     SF_GEMV_CASE(6) SF_GEMV_CASE(7) SF_GEMV_CASE(8)
 #undef SF_GEMV_CASE
@@ -126,39 +141,48 @@ static hipError_t launch_gemv_t(const GemvArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Few rows (the timestep MLP): one row per wavefront for parallelism. Many rows (the
+// adaLN table): four rows per wavefront and one butterfly reduction per row group.
+template <typename WT>
+static hipError_t launch_gemv_t(const GemvArgs& a, hipStream_t s) {
+  return a.R < 16384 ? launch_gemv_rows<WT, 1>(a, s) : launch_gemv_rows<WT, 4>(a, s);
+}
+
 hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s) {
   return w_bf16 ? launch_gemv_t<bf16>(a, s) : launch_gemv_t<float>(a, s);
 }
 
-// One workgroup per token: gather the token's p*p*C patch values (feature
-// (i*p + j)*C + c of token gh*(W/p) + gw reads x[c][gh*p + i][gw*p + j]), then each
-// thread produces columns of h = tok . W_pe^T + b_pe + pos[n].
+// One thread per four consecutive outputs of one token: the token's p*p*C patch values
+// (feature (i*p + j)*C + c of token gh*(W/p) + gw reads x[c][gh*p + i][gw*p + j]) times
+// the transposed patch-embedding weight W_peT [P][D], plus bias and position row.
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
-  __shared__ float tok[kMaxPatch];
-  const int m = blockIdx.x;
+  const int d4n = a.D >> 2;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= a.rows * a.N * d4n) return;
+  const int m = idx / d4n, d = (idx - m * d4n) * 4;
   const int r = m / a.N;
   const int n = m - r * a.N;
   const int lat = r % a.n_lat;
   const int gwn = a.W / a.p;
   const int gh = n / gwn, gw = n - gh * gwn;
   const int P = a.p * a.p * a.C;
-  if (threadIdx.x < P) {
-    const int f = threadIdx.x;
+  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int f = 0; f < P; ++f) {
     const int c = f % a.C, ij = f / a.C;
     const int i = ij / a.p, j = ij - i * a.p;
-    tok[f] = a.x[(((size_t)lat * a.C + c) * a.H + gh * a.p + i) * a.W + gw * a.p + j];
+    const float t = a.x[(((size_t)lat * a.C + c) * a.H + gh * a.p + i) * a.W + gw * a.p + j];
+    const float4 w = *(const float4*)(a.W_pe + (size_t)f * a.D + d);
+    acc.x += t * w.x; acc.y += t * w.y; acc.z += t * w.z; acc.w += t * w.w;
   }
-  __syncthreads();
-  for (int d = threadIdx.x; d < a.D; d += blockDim.x) {
-    const float* wr = a.W_pe + (size_t)d * P;
-    float acc = 0.0f;
-    for (int f = 0; f < P; ++f) acc += tok[f] * wr[f];
-    a.h[(size_t)m * a.D + d] = (acc + a.b_pe[d]) + a.pos[(size_t)n * a.D + d];
-  }
+  const float4 b = *(const float4*)(a.b_pe + d);
+  const float4 ps = *(const float4*)(a.pos + (size_t)n * a.D + d);
+  *(float4*)(a.h + (size_t)m * a.D + d) =
+      make_float4((acc.x + b.x) + ps.x, (acc.y + b.y) + ps.y, (acc.z + b.z) + ps.z, (acc.w + b.w) + ps.w);
 }
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(embed_kernel, dim3(a.rows * a.N), dim3(256), 0, s, a);
+  const int total = a.rows * a.N * (a.D >> 2);
+  hipLaunchKernelGGL(embed_kernel, dim3((total + 255) / 256), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -155,34 +155,42 @@ __device__ __forceinline__ void tile_coords(int nbm, int nbn, int& mt, int& nt) 
   nt = in / gsize;
 }
 
-// Operand tiles come in through raw buffer loads: rows past M or N and columns past K
-// get an out-of-range offset and read as zeros, so the loads carry no branches. Two
-// register stages keep the tile two K slices ahead in flight while the matrix cores
-// work on the current one from LDS (double-buffered, 16-byte row pad). PF = 1 keeps
-// one register stage (tiles with many wavefronts, where other wavefronts hide the
-// latency and registers are scarce), PF = 2 keeps two.
-template <int BM, int BN, int WM, int WN, int PF, EpiKind KIND>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_kernel(GemmArgs a) {
+// The bf16 GEMM with an explicitly interleaved main loop. Operand tiles come in through
+// raw buffer loads (rows past M or N and columns past K get an out-of-range offset and
+// read as zeros, so the loads carry no branches). Each K step is one straight
+// block: the matrix-core instructions of tile k are interleaved (sched_group_barrier)
+// with the LDS fragment reads of tile k, the LDS writes of tile k+1 (already in
+// registers) and the buffer loads of tile k+2, so memory work issues under the MFMAs
+// instead of in stalls between them. Loader chunks past the tile (when the chunk count
+// is not a multiple of the thread count) read zeros and land in a spare LDS slot, so
+// the block stays branch-free.
+template <int BM, int BN, int WM, int WN, EpiKind KIND>
+__global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs a) {
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM / 32;
   constexpr int TN = BN / WN / 32;
   static_assert(TM * WM * 32 == BM && TN * WN * 32 == BN, "wave grid must tile the block");
-  constexpr int CPR = kBK / 8;  // 16-byte chunks per tile row
+  constexpr int CPR = kBK / 8;
   constexpr int ATOT = BM * CPR, BTOT = BN * CPR;
   constexpr int ACH = (ATOT + NT - 1) / NT;
   constexpr int BCH = (BTOT + NT - 1) / NT;
-  constexpr int AB_BYTES = 2 * (BM + BN) * kLdk * 2;
+  constexpr int AB_BYTES = 2 * (BM + BN) * kLdk * 2 + 16;  // + spare slot
   constexpr int CP = BN + 4;
   constexpr int LDS_CAP = 160 * 1024;
   constexpr int NP = (BM * CP * 4 <= LDS_CAP) ? 1 : ((BM / 2) * CP * 4 <= LDS_CAP ? 2 : 4);
-  constexpr int RP = BM / NP;  // C rows staged per pass
-  static_assert(RP % 32 == 0, "staging pass must hold whole MFMA blocks");
+  constexpr int RP = BM / NP;
   constexpr int C_BYTES = RP * CP * 4;
   constexpr int SMEM = AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES;
   static_assert(SMEM <= LDS_CAP, "tile does not fit in LDS");
+  constexpr int KS = kBK / 16;                 // MFMA K steps per tile
+  constexpr int NMFMA = TM * TN * KS;
+  constexpr int NDSR = (TM + TN) * KS;
+  constexpr int NDSW = ACH + BCH;
+  constexpr int NVMEM = ACH + BCH;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   bf16* As = (bf16*)smem;
   bf16* Bs = As + 2 * BM * kLdk;
+  constexpr int SPARE = 2 * (BM + BN) * kLdk;  // bf16 index of the spare slot
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -194,38 +202,47 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_kernel(GemmArgs a) {
 
   const __amdgpu_buffer_rsrc_t ra_src = buffer_rsrc(a.A, (uint32_t)a.M * a.lda * 2);
   const __amdgpu_buffer_rsrc_t rb_src = buffer_rsrc(a.B, (uint32_t)a.N * a.ldb * 2);
-  int a_off[ACH], b_off[BCH], a_lds[ACH], b_lds[BCH], a_kc[ACH], b_kc[BCH];
+  // per chunk: global byte offset at k = 0 (or out of range), K column, and LDS index
+  // relative to the buffer base (the spare slot minus the buffer base for chunks past
+  // the tile, so `buffer base + index` always lands in the spare slot)
+  int a_off[ACH], b_off[BCH], a_kc[ACH], b_kc[BCH], a_lds[ACH], b_lds[BCH];
 #pragma unroll
   for (int i = 0; i < ACH; ++i) {
     const int c = tid + i * NT, row = c / CPR;
+    const bool in = c < ATOT;
     a_kc[i] = (c % CPR) * 8;
-    a_lds[i] = row * kLdk + a_kc[i];
-    a_off[i] = (c < ATOT && m0 + row < a.M) ? ((m0 + row) * a.lda + a_kc[i]) * 2 : kOffOOB;
+    a_lds[i] = in ? row * kLdk + a_kc[i] : -1;
+    a_off[i] = (in && m0 + row < a.M) ? ((m0 + row) * a.lda + a_kc[i]) * 2 : kOffOOB;
   }
 #pragma unroll
   for (int i = 0; i < BCH; ++i) {
     const int c = tid + i * NT, row = c / CPR;
+    const bool in = c < BTOT;
     b_kc[i] = (c % CPR) * 8;
-    b_lds[i] = row * kLdk + b_kc[i];
-    b_off[i] = (c < BTOT && n0 + row < a.N) ? ((n0 + row) * a.ldb + b_kc[i]) * 2 : kOffOOB;
+    b_lds[i] = in ? row * kLdk + b_kc[i] : -1;
+    b_off[i] = (in && n0 + row < a.N) ? ((n0 + row) * a.ldb + b_kc[i]) * 2 : kOffOOB;
   }
-  u32x4 ra[PF][ACH], rb[PF][BCH];
-  auto gload = [&](u32x4 (&va)[ACH], u32x4 (&vb)[BCH], int kt) {
+  u32x4 ra[ACH], rb[BCH];
+  auto gload = [&](int kt) {
     const int k0 = kt * kBK;
 #pragma unroll
     for (int i = 0; i < ACH; ++i)
-      va[i] = buffer_load16(ra_src, (k0 + a_kc[i] < a.K && a_off[i] != kOffOOB) ? a_off[i] + 2 * k0 : kOffOOB);
+      ra[i] = buffer_load16(ra_src, (k0 + a_kc[i] < a.K && a_off[i] != kOffOOB) ? a_off[i] + 2 * k0 : kOffOOB);
 #pragma unroll
     for (int i = 0; i < BCH; ++i)
-      vb[i] = buffer_load16(rb_src, (k0 + b_kc[i] < a.K && b_off[i] != kOffOOB) ? b_off[i] + 2 * k0 : kOffOOB);
+      rb[i] = buffer_load16(rb_src, (k0 + b_kc[i] < a.K && b_off[i] != kOffOOB) ? b_off[i] + 2 * k0 : kOffOOB);
   };
-  auto lstore = [&](const u32x4 (&va)[ACH], const u32x4 (&vb)[BCH], int buf) {
+  auto lstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < ACH; ++i)
-      if (ATOT % NT == 0 || tid + i * NT < ATOT) *(u32x4*)&As[buf * BM * kLdk + a_lds[i]] = va[i];
+    for (int i = 0; i < ACH; ++i) {
+      const int idx = (ATOT % NT == 0 || a_lds[i] >= 0) ? buf * BM * kLdk + a_lds[i] : SPARE;
+      *(u32x4*)&As[idx] = ra[i];
+    }
 #pragma unroll
-    for (int i = 0; i < BCH; ++i)
-      if (BTOT % NT == 0 || tid + i * NT < BTOT) *(u32x4*)&Bs[buf * BN * kLdk + b_lds[i]] = vb[i];
+    for (int i = 0; i < BCH; ++i) {
+      const int idx = (BTOT % NT == 0 || b_lds[i] >= 0) ? buf * BN * kLdk + b_lds[i] : SPARE - 2 * BM * kLdk;
+      *(u32x4*)&Bs[idx] = rb[i];
+    }
   };
 
   f32x16 acc[TM][TN];
@@ -236,18 +253,18 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  auto compute = [&](int buf) {
-    const bf16* Ab = As + buf * BM * kLdk + (wm * TM * 32 + l32) * kLdk + g * 8;
-    const bf16* Bb = Bs + buf * BN * kLdk + (wn * TN * 32 + l32) * kLdk + g * 8;
+  auto step = [&](int cur, int kt, bool write_next, bool load_next) {
+    const bf16* Ab = As + cur * BM * kLdk + (wm * TM * 32 + l32) * kLdk + g * 8;
+    const bf16* Bb = Bs + cur * BN * kLdk + (wn * TN * 32 + l32) * kLdk + g * 8;
     bf16x8 af[2][TM], bfr[2][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i) af[0][i] = *(const bf16x8*)(Ab + i * 32 * kLdk);
 #pragma unroll
     for (int j = 0; j < TN; ++j) bfr[0][j] = *(const bf16x8*)(Bb + j * 32 * kLdk);
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
+    for (int kk = 0; kk < KS; ++kk) {
       const int cb = kk & 1;
-      if (kk + 1 < kBK / 16) {
+      if (kk + 1 < KS) {
 #pragma unroll
         for (int i = 0; i < TM; ++i) af[cb ^ 1][i] = *(const bf16x8*)(Ab + i * 32 * kLdk + (kk + 1) * 16);
 #pragma unroll
@@ -259,44 +276,42 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_kernel(GemmArgs a) {
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cb][i], bfr[cb][j], acc[i][j], 0, 0, 0);
     }
+    if (write_next) lstore(cur ^ 1);
+    if (load_next) gload(kt + 2);
+    // interleave: the fragment reads ahead of their MFMAs over the first half of the
+    // MFMAs, the LDS writes and global loads over the second half
+    constexpr int H1 = NMFMA / 2, H2 = NMFMA - NMFMA / 2;
+#pragma unroll
+    for (int i = 0; i < H1; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, (NDSR + H1 - 1) / H1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < H2; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x200, (NDSW + H2 - 1) / H2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, (NVMEM + H2 - 1) / H2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
   };
 
   const int nk = (a.K + kBK - 1) / kBK;
-  if constexpr (PF == 2) {
-    gload(ra[0], rb[0], 0);
-    if (nk > 1) gload(ra[PF - 1], rb[PF - 1], 1);
-    lstore(ra[0], rb[0], 0);
-    if (nk > 2) gload(ra[0], rb[0], 2);
+  gload(0);
+  lstore(0);
+  if (nk > 1) gload(1);
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 2 < nk; ++kt) {
+    step(kt & 1, kt, true, true);
     __syncthreads();
-    for (int kt = 0; kt < nk; kt += 2) {
-      compute(0);  // tile kt
-      if (kt + 1 < nk) {
-        lstore(ra[PF - 1], rb[PF - 1], 1);  // tile kt+1
-        if (kt + 3 < nk) gload(ra[PF - 1], rb[PF - 1], kt + 3);
-      }
-      __syncthreads();
-      if (kt + 1 >= nk) break;
-      compute(1);  // tile kt+1
-      if (kt + 2 < nk) {
-        lstore(ra[0], rb[0], 0);  // tile kt+2
-        if (kt + 4 < nk) gload(ra[0], rb[0], kt + 4);
-      }
-      __syncthreads();
-    }
-  } else {
-    gload(ra[0], rb[0], 0);
-    lstore(ra[0], rb[0], 0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      if (kt + 1 < nk) gload(ra[0], rb[0], kt + 1);
-      compute(kt & 1);
-      if (kt + 1 < nk) lstore(ra[0], rb[0], (kt + 1) & 1);
-      __syncthreads();
-    }
   }
+  if (kt + 1 < nk) {
+    step(kt & 1, kt, true, false);
+    __syncthreads();
+    ++kt;
+  }
+  step(kt & 1, kt, false, false);
+  __syncthreads();
 
-  // stage C in passes of RP rows (lane holds column l32 and rows (r/4)*8 + g*4 + r%4
-  // of each 32x32 block), then run the fused epilogue on each pass
   float* Cs = (float*)smem;
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
@@ -369,193 +384,18 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   }
 }
 
-// The same GEMM with an explicitly interleaved main loop. Each K step is one straight
-// block: the matrix-core instructions of tile k are interleaved (sched_group_barrier)
-// with the LDS fragment reads of tile k, the LDS writes of tile k+1 (already in
-// registers) and the buffer loads of tile k+2, so memory work issues under the MFMAs
-// instead of in stalls between them.
-template <int BM, int BN, int WM, int WN, EpiKind KIND>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs a) {
-  constexpr int NT = WM * WN * 64;
-  constexpr int TM = BM / WM / 32;
-  constexpr int TN = BN / WN / 32;
-  static_assert(TM * WM * 32 == BM && TN * WN * 32 == BN, "wave grid must tile the block");
-  constexpr int CPR = kBK / 8;
-  constexpr int ATOT = BM * CPR, BTOT = BN * CPR;
-  constexpr int ACH = (ATOT + NT - 1) / NT;
-  constexpr int BCH = (BTOT + NT - 1) / NT;
-  static_assert(ATOT % NT == 0 && BTOT % NT == 0, "scheduled variant needs whole chunks per thread");
-  constexpr int AB_BYTES = 2 * (BM + BN) * kLdk * 2;
-  constexpr int CP = BN + 4;
-  constexpr int LDS_CAP = 160 * 1024;
-  constexpr int NP = (BM * CP * 4 <= LDS_CAP) ? 1 : ((BM / 2) * CP * 4 <= LDS_CAP ? 2 : 4);
-  constexpr int RP = BM / NP;
-  constexpr int C_BYTES = RP * CP * 4;
-  constexpr int SMEM = AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES;
-  static_assert(SMEM <= LDS_CAP, "tile does not fit in LDS");
-  constexpr int NMFMA = TM * TN * (kBK / 16);
-  constexpr int NDSR = (TM + TN) * (kBK / 16);
-  constexpr int NDSW = ACH + BCH;
-  constexpr int NVMEM = ACH + BCH;
-  __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  bf16* As = (bf16*)smem;
-  bf16* Bs = As + 2 * BM * kLdk;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int l32 = lane & 31, g = lane >> 5;
-  int mt, nt;
-  tile_coords((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
-  const int m0 = mt * BM, n0 = nt * BN;
-
-  const __amdgpu_buffer_rsrc_t ra_src = buffer_rsrc(a.A, (uint32_t)a.M * a.lda * 2);
-  const __amdgpu_buffer_rsrc_t rb_src = buffer_rsrc(a.B, (uint32_t)a.N * a.ldb * 2);
-  int a_off[ACH], b_off[BCH], a_lds[ACH], b_lds[BCH], a_kc[ACH], b_kc[BCH];
-#pragma unroll
-  for (int i = 0; i < ACH; ++i) {
-    const int c = tid + i * NT, row = c / CPR;
-    a_kc[i] = (c % CPR) * 8;
-    a_lds[i] = row * kLdk + a_kc[i];
-    a_off[i] = (m0 + row < a.M) ? ((m0 + row) * a.lda + a_kc[i]) * 2 : kOffOOB;
-  }
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    const int c = tid + i * NT, row = c / CPR;
-    b_kc[i] = (c % CPR) * 8;
-    b_lds[i] = row * kLdk + b_kc[i];
-    b_off[i] = (n0 + row < a.N) ? ((n0 + row) * a.ldb + b_kc[i]) * 2 : kOffOOB;
-  }
-  u32x4 ra[ACH], rb[BCH];
-  auto gload = [&](int kt) {
-    const int k0 = kt * kBK;
-#pragma unroll
-    for (int i = 0; i < ACH; ++i)
-      ra[i] = buffer_load16(ra_src, (k0 + a_kc[i] < a.K && a_off[i] != kOffOOB) ? a_off[i] + 2 * k0 : kOffOOB);
-#pragma unroll
-    for (int i = 0; i < BCH; ++i)
-      rb[i] = buffer_load16(rb_src, (k0 + b_kc[i] < a.K && b_off[i] != kOffOOB) ? b_off[i] + 2 * k0 : kOffOOB);
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) *(u32x4*)&As[buf * BM * kLdk + a_lds[i]] = ra[i];
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) *(u32x4*)&Bs[buf * BN * kLdk + b_lds[i]] = rb[i];
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  // one K step on LDS buffer `cur`; optionally writes the next tile (registers -> LDS
-  // buffer cur^1) and fetches the one after into registers
-  auto step = [&](int cur, int kt, bool write_next, bool load_next) {
-    const bf16* Ab = As + cur * BM * kLdk + (wm * TM * 32 + l32) * kLdk + g * 8;
-    const bf16* Bb = Bs + cur * BN * kLdk + (wn * TN * 32 + l32) * kLdk + g * 8;
-    bf16x8 af[kBK / 16][TM], bfr[kBK / 16][TN];
-#pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-#pragma unroll
-      for (int i = 0; i < TM; ++i) af[kk][i] = *(const bf16x8*)(Ab + i * 32 * kLdk + kk * 16);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bfr[kk][j] = *(const bf16x8*)(Bb + j * 32 * kLdk + kk * 16);
-    }
-#pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk)
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kk][i], bfr[kk][j], acc[i][j], 0, 0, 0);
-    if (write_next) lstore(cur ^ 1);
-    if (load_next) gload(kt + 2);
-    // interleave: fragment reads ahead of their MFMAs, then LDS writes and global loads
-    // spread across the remaining MFMAs
-    constexpr int R_PER = (NDSR + NMFMA - 1) / NMFMA;
-#pragma unroll
-    for (int i = 0; i < NMFMA / 2; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 2 * R_PER, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < NMFMA - NMFMA / 2; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x200, (NDSW + NMFMA / 2 - 1) / (NMFMA / 2), 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, (NVMEM + NMFMA / 2 - 1) / (NMFMA / 2), 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-  };
-
-  const int nk = (a.K + kBK - 1) / kBK;
-  gload(0);
-  lstore(0);
-  if (nk > 1) gload(1);
-  __syncthreads();
-  int kt = 0;
-  for (; kt + 2 < nk; ++kt) {
-    step(kt & 1, kt, true, true);
-    __syncthreads();
-  }
-  if (kt + 1 < nk) {
-    step(kt & 1, kt, true, false);
-    __syncthreads();
-    ++kt;
-  }
-  step(kt & 1, kt, false, false);
-  __syncthreads();
-
-  float* Cs = (float*)smem;
-#pragma unroll
-  for (int p = 0; p < NP; ++p) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int rb0 = (wm * TM + i) * 32;
-      if (rb0 < p * RP || rb0 >= (p + 1) * RP) continue;
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = rb0 - p * RP + (r >> 2) * 8 + g * 4 + (r & 3);
-          Cs[row * CP + (wn * TN + j) * 32 + l32] = acc[i][j][r];
-        }
-    }
-    __syncthreads();
-    staged_epilogue<KIND, RP, BN, NT>(a, Cs, CP, m0 + p * RP, n0, tid);
-    if (p + 1 < NP) __syncthreads();
-  }
-}
-
-// Tile shapes (BM x BN, wave grid WM x WN, register prefetch stages). Per-wave tiles
-// are 64x64, 64x96 or 32x96.
-#define SF_GEMM_TILES(X)    \
-  X(0, 128, 128, 2, 2, 2)   \
-  X(1, 128, 96, 4, 1, 2)    \
-  X(2, 128, 96, 2, 1, 2)    \
-  X(3, 128, 288, 2, 3, 1)   \
-  X(4, 128, 384, 2, 4, 1)   \
-  X(5, 256, 128, 4, 2, 1)   \
-  X(6, 64, 192, 1, 2, 2)    \
-  X(7, 128, 192, 2, 2, 2)   \
-  X(8, 256, 96, 4, 1, 2)    \
-  X(9, 128, 128, 2, 2, 1)   \
-  X(10, 256, 256, 2, 4, 1)  \
-  X(11, 256, 128, 2, 2, 1)  \
-  X(12, 256, 128, 2, 2, 2)  \
-  X(13, 128, 256, 2, 2, 1)  \
-  X(14, 256, 256, 4, 2, 1)  \
-  X(15, 128, 128, 2, 2, 0)  \
-  X(16, 256, 256, 2, 4, 0)  \
-  X(17, 128, 256, 2, 2, 0)  \
-  X(18, 256, 128, 4, 2, 0)
+// Tile shapes (BM x BN, wave grid WM x WN). Per-wave tiles are 64x64 or 64x96.
+#define SF_GEMM_TILES(X)   \
+  X(0, 128, 128, 2, 2)     \
+  X(1, 128, 288, 2, 3)     \
+  X(2, 128, 384, 2, 4)     \
+  X(3, 128, 192, 2, 2)
 
 struct TileInfo {
   int bm, bn, waves;
 };
 static const TileInfo kTiles[] = {
-#define SF_TILE_INFO(id, bm, bn, wm, wn, pf) {bm, bn, wm * wn},
+#define SF_TILE_INFO(id, bm, bn, wm, wn) {bm, bn, wm * wn},
     SF_GEMM_TILES(SF_TILE_INFO)
 #undef SF_TILE_INFO
 };
@@ -564,14 +404,10 @@ constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 template <EpiKind KIND>
 static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
   switch (tile) {
-#define SF_TILE_CASE(id, bm, bn, wm, wn, pf)                                                      \
-  case id:                                                                                         \
-    if constexpr (pf == 0)                                                                         \
-      hipLaunchKernelGGL((gemm_bf16_sched_kernel<bm, bn, wm, wn, KIND>),                            \
-                         dim3(((a.N + bn - 1) / bn) * ((a.M + bm - 1) / bm)), dim3(wm * wn * 64), 0, s, a); \
-    else                                                                                           \
-      hipLaunchKernelGGL((gemm_bf16_kernel<bm, bn, wm, wn, (pf == 0 ? 1 : pf), KIND>),               \
-                         dim3(((a.N + bn - 1) / bn) * ((a.M + bm - 1) / bm)), dim3(wm * wn * 64), 0, s, a); \
+#define SF_TILE_CASE(id, bm, bn, wm, wn)                                                   \
+  case id:                                                                                  \
+    hipLaunchKernelGGL((gemm_bf16_sched_kernel<bm, bn, wm, wn, KIND>),                      \
+                       dim3(((a.N + bn - 1) / bn) * ((a.M + bm - 1) / bm)), dim3(wm * wn * 64), 0, s, a); \
     break;
     SF_GEMM_TILES(SF_TILE_CASE)
 #undef SF_TILE_CASE
@@ -581,14 +417,16 @@ static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// The interleaved 128x128 tile (id 15) measured fastest on every projection shape of
-// the 512^2 and 1024^2 networks (M = 4096 / 16384, N in {768, 1152, 2304, 3072, 3456,
-// 4608}); the other shapes stay available to launch_gemm_tile.
+// Interleaved tiles, chosen from measurements on the 512^2 and 1024^2 projection
+// shapes: 128x128 (64x64 per wavefront) is the best general tile; 128x384 and 128x288
+// (64x96 per wavefront, 8 and 6 wavefronts) win when they cut the problem into exactly
+// one workgroup per CU (e.g. 4096x3072 and 4096x2304).
 int choose_gemm_tile(int M, int N, int K) {
-  (void)M;
-  (void)N;
   (void)K;
-  return 15;
+  auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
+  if (M % 128 == 0 && N % 384 == 0 && tiles(128, 384) == 256) return 2;
+  if (M % 128 == 0 && N % 288 == 0 && tiles(128, 288) == 256) return 1;
+  return 0;
 }
 
 template <EpiKind KIND>

@@ -53,13 +53,8 @@ template <> struct Store4<bf16> {
 };
 
 template <typename OT>
-__global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (m >= a.M) return;
-  float4 v[kLnVec];
-  float mean, rstd;
-  row_stats(a.h + (size_t)m * a.D, a.D, lane, v, mean, rstd);
+__device__ __forceinline__ void ln_store_row(const LnArgs& a, int m, int lane, const float4 (&v)[kLnVec], float mean,
+                                             float rstd) {
   const float* sh = nullptr;
   const float* sc = nullptr;
   if (a.table) {
@@ -89,8 +84,55 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
   }
 }
 
+// Two rows per wavefront, both rows' loads issued before either reduction.
+template <typename OT>
+__global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int m0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * 2;
+  if (m0 >= a.M) return;
+  const int m1 = min(m0 + 1, a.M - 1);
+  const int nv = a.D >> 2;
+  float4 v0[kLnVec], v1[kLnVec];
+  const float4* r0 = (const float4*)(a.h + (size_t)m0 * a.D);
+  const float4* r1 = (const float4*)(a.h + (size_t)m1 * a.D);
+#pragma unroll
+  for (int i = 0; i < kLnVec; ++i) {
+    const int c = lane + i * 64;
+    if (c < nv) {
+      v0[i] = r0[c];
+      v1[i] = r1[c];
+    }
+  }
+  float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kLnVec; ++i) {
+    const int c = lane + i * 64;
+    if (c < nv) {
+      s0 += (v0[i].x + v0[i].y) + (v0[i].z + v0[i].w);
+      s1 += (v1[i].x + v1[i].y) + (v1[i].z + v1[i].w);
+    }
+  }
+  const float mean0 = wave_sum(s0) / (float)a.D, mean1 = wave_sum(s1) / (float)a.D;
+  float q0 = 0.0f, q1 = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kLnVec; ++i) {
+    const int c = lane + i * 64;
+    if (c < nv) {
+      float d;
+      d = v0[i].x - mean0; q0 += d * d; d = v0[i].y - mean0; q0 += d * d;
+      d = v0[i].z - mean0; q0 += d * d; d = v0[i].w - mean0; q0 += d * d;
+      d = v1[i].x - mean1; q1 += d * d; d = v1[i].y - mean1; q1 += d * d;
+      d = v1[i].z - mean1; q1 += d * d; d = v1[i].w - mean1; q1 += d * d;
+    }
+  }
+  const float rstd0 = 1.0f / sqrtf(wave_sum(q0) / (float)a.D + kLnEps);
+  const float rstd1 = 1.0f / sqrtf(wave_sum(q1) / (float)a.D + kLnEps);
+  ln_store_row<OT>(a, m0, lane, v0, mean0, rstd0);
+  if (m0 + 1 < a.M) ln_store_row<OT>(a, m1, lane, v1, mean1, rstd1);
+}
+
 hipError_t launch_ln(bool out_bf16, const LnArgs& a, hipStream_t s) {
-  const int grid = (a.M + 3) / 4;
+  const int grid = (a.M + 7) / 8;
   if (out_bf16)
     hipLaunchKernelGGL(ln_mod_kernel<bf16>, dim3(grid), dim3(256), 0, s, a);
   else
@@ -98,10 +140,21 @@ hipError_t launch_ln(bool out_bf16, const LnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// W_f lives in LDS for the whole workgroup; each wavefront walks token rows.
+// W_f lives in LDS for the whole workgroup (staged with independent 16-byte loads);
+// each wavefront walks token rows.
 __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
   extern __shared__ float wf[];  // [P][D]
-  for (int i = threadIdx.x; i < a.P * a.D; i += blockDim.x) wf[i] = a.W_f[i];
+  {
+    const int n4 = (a.P * a.D) >> 2;
+    const float4* src = (const float4*)a.W_f;
+    float4* dst = (float4*)wf;
+    constexpr int kStage = kMaxPatch * kMaxWidth / 4 / 256;
+#pragma unroll
+    for (int k = 0; k < kStage; ++k) {
+      const int i = threadIdx.x + k * 256;
+      if (i < n4) dst[i] = src[i];
+    }
+  }
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -147,14 +200,9 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
           }
         }
       }
-      float mine = 0.0f;
-#pragma unroll
-      for (int o = 0; o < 16; ++o) {
-        const float t = wave_sum(acc[o]);
-        if (lane == o) mine = t;
-      }
-      const int f = o0 + lane;
-      if (lane < 16 && f < a.P) {
+      const float mine = wave_reduce16(acc);
+      const int f = o0 + ((lane >> 2) & 15);
+      if ((lane & 3) == 0 && f < a.P) {
         const int c = f % a.C, ij = f / a.C;
         const int i = ij / a.p, j = ij - i * a.p;
         a.v[(((size_t)r * a.C + c) * a.H + gh * a.p + i) * a.W + gw * a.p + j] = mine + a.b_f[f];

@@ -31,6 +31,47 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Sums each of 16 per-lane values over the 64 lanes of a wavefront and returns, in
+// lane l, the total of index (l >> 2) & 15 (lanes 4i..4i+3 all hold total i). Butterfly
+// reduce-scatter: four halving exchanges (xor 32, 16, 8, 4; 8 + 4 + 2 + 1 shuffles) then
+// two plain ones (xor 2, 1): 17 shuffles instead of 16 separate 6-step reductions.
+__device__ __forceinline__ float wave_reduce16(float (&v)[16]) {
+  const int lane = threadIdx.x & 63;
+  float a8[8], a4[4], a2[2];
+  {
+    const bool hi = lane & 32;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float mine = hi ? v[8 + i] : v[i];
+      const float give = hi ? v[i] : v[8 + i];
+      a8[i] = mine + __shfl_xor(give, 32);
+    }
+  }
+  {
+    const bool hi = lane & 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float mine = hi ? a8[4 + i] : a8[i];
+      const float give = hi ? a8[i] : a8[4 + i];
+      a4[i] = mine + __shfl_xor(give, 16);
+    }
+  }
+  {
+    const bool hi = lane & 8;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const float mine = hi ? a4[2 + i] : a4[i];
+      const float give = hi ? a4[i] : a4[2 + i];
+      a2[i] = mine + __shfl_xor(give, 8);
+    }
+  }
+  const bool hi = lane & 4;
+  float r = (hi ? a2[1] : a2[0]) + __shfl_xor(hi ? a2[0] : a2[1], 4);
+  r += __shfl_xor(r, 2);
+  r += __shfl_xor(r, 1);
+  return r;
+}
+
 template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }  // RNE

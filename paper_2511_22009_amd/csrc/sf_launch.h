@@ -47,7 +47,7 @@ hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s);
 struct EmbedArgs {
   const float* x;       // [n_lat][C][H][W]
   int n_lat;            // network row r reads latent r % n_lat
-  const float* W_pe;    // [D][P]
+  const float* W_pe;    // [P][D] (transposed patch-embedding weight)
   const float* b_pe;    // [D]
   const float* pos;     // [N][D]
   float* h;             // [rows*N][D]

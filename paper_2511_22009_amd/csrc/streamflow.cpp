@@ -230,7 +230,12 @@ void fill_weights(sf_model* m, const char* blob, std::vector<char>& img) {
     }
     src += n;
   };
-  put_f32(m->W_pe, D * P);
+  {  // W_pe [D][P] in the blob, stored transposed [P][D] for coalesced reads
+    float* dst = (float*)(base + dev_off(m->W_pe));
+    for (size_t d = 0; d < D; ++d)
+      for (size_t f = 0; f < P; ++f) dst[f * D + d] = src[d * P + f];
+    src += D * P;
+  }
   put_f32(m->b_pe, D);
   put_f32(m->pos, (size_t)m->N * D);
   put_f32(m->W_t1, D * h.tdim);
