@@ -30,6 +30,26 @@ MI355X_PEAK_BF16_TFLOPS = 2500.0
 MI355X_PEAK_FP32_TFLOPS = 157.3
 MI355X_HBM_GBS = 8000.0
 
+# HBM bytes per launch of a kernel class, from two rocprofv3 --pmc passes (FETCH_SIZE,
+# then WRITE_SIZE, KiB per dispatch) over `bench.py --steps 5 --warmup 2 --no-cpu
+# --no-sequential --copy-calibration`, each scaled by what the same counter reads for a
+# plain 256 MiB elementwise copy (FETCH_SIZE x 2.000, WRITE_SIZE x 1.000). An entry holds
+# only for the kernel sources it was measured on (hash below); otherwise traffic is null.
+KERNEL_SOURCES = ("k_gemm.hip", "sf_device.h", "sf_launch.h")
+TRAFFIC = {
+    ("s512", "bf16", "FC2"): {"bytes": 94497912, "sources": "3f3ea8b56adb86c5",
+                              "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
+}
+
+
+def kernel_sources_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2511_22009_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
 
 def class_work(cfg, kc, rows):
     """Algorithmic FLOPs of ONE launch of kernel class kc (GEMM classes and attention)."""
@@ -78,6 +98,11 @@ def main():
     ap.add_argument("--config", default="s512")
     ap.add_argument("--precision", default="bf16", choices=["bf16", "fp32"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-sequential", action="store_true",
+                    help="skip the one-latent-at-a-time comparison run (keeps profiles to the batched step)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed steps, run a plain 256 MiB elementwise copy kernel (three times) "
+                         "whose FETCH_SIZE / WRITE_SIZE counters scale the kernels' HBM traffic")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested): the stream step has no "
@@ -146,24 +171,28 @@ def main():
     avg_launch_s = dom_ms / 1e3 / max(dom_n, 1)
     achieved = work / avg_launch_s / 1e12
     peak = MI355X_PEAK_BF16_TFLOPS if args.precision == "bf16" else MI355X_PEAK_FP32_TFLOPS
+    tr = TRAFFIC.get((cfg.name, args.precision, dom.name))
+    traffic = tr["bytes"] if tr and tr["sources"] == kernel_sources_hash() else None
     gemm_ms = sum(breakdown[k]["ms_per_step"] for k in ("QKV", "PROJ", "FC1", "FC2") if k in breakdown)
     gemm_tflops = cfg.gemm_flops_per_step() / (gemm_ms / 1e3) / 1e12 if gemm_ms else None
 
     # the same kernels one latent at a time (no stream batching): K network calls per image
-    seq_steps = max(4, args.steps // 10)
-    x1 = x[:1].clone()
-    done1 = torch.empty_like(done)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    cond1 = None if cond is None else Cond(cond.ctx[:1], cond.null_ctx, cond.guidance)
-    for i in range(seq_steps):
-        for s in range(K):
-            # a one-slot queue: the updated latent leaves through `done1` and, until the
-            # image is finished, re-enters slot 0 as the "fresh" latent
-            z = done1 if s < K - 1 else pool[i % pool.shape[0]]
-            m.stream_step(x1, t[s:s + 1], dt[s:s + 1], 1, z, done1, cond1, stream)
-    torch.cuda.synchronize()
-    seq_img_s = seq_steps / (time.perf_counter() - t1)
+    seq_img_s = None
+    if not args.no_sequential:
+        seq_steps = max(4, args.steps // 10)
+        x1 = x[:1].clone()
+        done1 = torch.empty_like(done)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        cond1 = None if cond is None else Cond(cond.ctx[:1], cond.null_ctx, cond.guidance)
+        for i in range(seq_steps):
+            for s in range(K):
+                # a one-slot queue: the updated latent leaves through `done1` and, until the
+                # image is finished, re-enters slot 0 as the "fresh" latent
+                z = done1 if s < K - 1 else pool[i % pool.shape[0]]
+                m.stream_step(x1, t[s:s + 1], dt[s:s + 1], 1, z, done1, cond1, stream)
+        torch.cuda.synchronize()
+        seq_img_s = seq_steps / (time.perf_counter() - t1)
 
     out = {
         "metric": METRIC,
@@ -197,7 +226,9 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": achieved / peak,
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+            "traffic_profile": tr["profile"] if traffic else None,
             "flops_per_launch": work,
             "avg_launch_us": avg_launch_s * 1e6,
             "launches_timed": dom_n,
@@ -205,6 +236,13 @@ def main():
         "breakdown_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in breakdown.items()},
     }
     m.close()
+    if args.copy_calibration:
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)  # an elementwise kernel: reads and writes 256 MiB
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = src.numel() * 4
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(out))

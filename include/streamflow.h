@@ -181,11 +181,13 @@ enum {
   SF_KC_COUNT
 };
 
-/* Test and bench hook: while enabled, every launch of kernel class `kc` is bracketed
- * by a pair of HIP events recorded on the launch stream (at most 16384 launches are
- * recorded; later ones are counted but not timed). sf_timing_read waits for the
- * recorded events, returns the summed milliseconds and the number of timed launches,
- * and clears the record. */
+/* Test and bench hook: while enabled, every launch of kernel class `kc` is timed by a
+ * pair of HIP events. For a class that is one kernel the events are attached to that
+ * kernel's dispatch (its own start and end); SF_KC_TEMB and SF_KC_CROSS, which launch
+ * several kernels, are bracketed by events recorded on the launch stream. At most 4096
+ * launches per class are recorded; later ones are counted but not timed. sf_timing_read
+ * waits for the recorded events, returns the summed milliseconds and the number of
+ * timed launches, and clears the record. */
 int sf_timing_enable(sf_model* m, int kc, int enable);
 int sf_timing_read(sf_model* m, int kc, double* total_ms, long* launches);
 

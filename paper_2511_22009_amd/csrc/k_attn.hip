@@ -268,7 +268,7 @@ bool attention_supports(int dh) { return dh >= 8 && dh <= 128 && dh % 8 == 0; }
 template <int DHC, int DB>
 static void launch_bf16_inst(const AttnArgs& a, hipStream_t s) {
   dim3 grid(((a.Nq + kQB - 1) / kQB) * a.heads * a.rows);
-  hipLaunchKernelGGL((attn_bf16_kernel<DHC, DB>), grid, dim3(256), 0, s, a);
+  launch((attn_bf16_kernel<DHC, DB>), grid, dim3(256), 0, s, a);
 }
 
 hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
@@ -289,11 +289,11 @@ hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
   } else {
     dim3 grid((a.Nq + 127) / 128, a.heads, a.rows);
     if (a.dh <= 32)
-      hipLaunchKernelGGL(attn_f32_kernel<32>, grid, dim3(128), 0, s, a);
+      launch(attn_f32_kernel<32>, grid, dim3(128), 0, s, a);
     else if (a.dh <= 64)
-      hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(128), 0, s, a);
+      launch(attn_f32_kernel<64>, grid, dim3(128), 0, s, a);
     else
-      hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(128), 0, s, a);
+      launch(attn_f32_kernel<128>, grid, dim3(128), 0, s, a);
   }
   return hipGetLastError();
 }

@@ -132,7 +132,7 @@ static hipError_t launch_gemv_rows(const GemvArgs& a, hipStream_t s) {
   if (grid > 2048) grid = 2048;
   switch (nch) {
 #define SF_GEMV_CASE(n) \
-  case n: hipLaunchKernelGGL((gemv_kernel<WT, n, ROWS>), dim3(grid), dim3(256), 0, s, a); break;
+  case n: launch((gemv_kernel<WT, n, ROWS>), dim3(grid), dim3(256), 0, s, a); break;
     SF_GEMV_CASE(1) SF_GEMV_CASE(2) SF_GEMV_CASE(3) SF_GEMV_CASE(4) SF_GEMV_CASE(5)
     SF_GEMV_CASE(6) SF_GEMV_CASE(7) SF_GEMV_CASE(8)
 #undef SF_GEMV_CASE
@@ -182,7 +182,7 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   const int total = a.rows * a.N * (a.D >> 2);
-  hipLaunchKernelGGL(embed_kernel, dim3((total + 255) / 256), dim3(256), 0, s, a);
+  launch(embed_kernel, dim3((total + 255) / 256), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -205,10 +205,10 @@ hipError_t launch_ctx_assemble(bool use_bf16, const float* ctx, const float* nul
   int grid = (int)(((size_t)rows * per_row + 255) / 256);
   if (grid > 4096) grid = 4096;
   if (use_bf16)
-    hipLaunchKernelGGL(ctx_assemble_kernel<bf16>, dim3(grid), dim3(256), 0, s, ctx, null_ctx,
+    launch(ctx_assemble_kernel<bf16>, dim3(grid), dim3(256), 0, s, ctx, null_ctx,
                        n_cond, rows, per_row, (bf16*)out);
   else
-    hipLaunchKernelGGL(ctx_assemble_kernel<float>, dim3(grid), dim3(256), 0, s, ctx, null_ctx,
+    launch(ctx_assemble_kernel<float>, dim3(grid), dim3(256), 0, s, ctx, null_ctx,
                        n_cond, rows, per_row, (float*)out);
   return hipGetLastError();
 }

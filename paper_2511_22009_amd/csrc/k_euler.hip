@@ -40,7 +40,7 @@ __global__ __launch_bounds__(256) void euler_shift_kernel(EulerArgs a) {
 
 hipError_t launch_euler_shift(const EulerArgs& a, hipStream_t s) {
   const int n4 = a.E >> 2;
-  hipLaunchKernelGGL(euler_shift_kernel, dim3((n4 + 255) / 256), dim3(256), 0, s, a);
+  launch(euler_shift_kernel, dim3((n4 + 255) / 256), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -56,7 +56,7 @@ __global__ __launch_bounds__(256) void cfg_combine_kernel(const float* v, int B,
 
 hipError_t launch_cfg_combine(const float* v, int B, int E, float w, float* v_out, hipStream_t s) {
   const size_t total = (size_t)B * (E >> 2);
-  hipLaunchKernelGGL(cfg_combine_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, v, B, E, w, v_out);
+  launch(cfg_combine_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, v, B, E, w, v_out);
   return hipGetLastError();
 }
 

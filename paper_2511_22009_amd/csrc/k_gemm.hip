@@ -39,7 +39,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int m, int n, float 
     OT* const p_qk = (OT*)(which == 0 ? a.q : a.k);
     OT* const dst = which >= 2 ? (OT*)a.vT + i_v : p_qk + i_qk;
     *dst = from_f32<OT>(val);
-  } else if constexpr (KIND == EPI_RES_GATE) {
+  } else if constexpr (KIND == EPI_RES_GATE || KIND == EPI_RES_GATE_MLP) {
     const int r = (int)fdiv((uint32_t)m, a.div_ntok);
     const int slot = r < a.n_slots ? r : r - a.n_slots;
     const float g = a.table[(size_t)slot * a.ldt + a.gate_off + n];
@@ -87,7 +87,7 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const float* 
       const int tok = m - r * a.ntok;
       bf16* base = (bf16*)(which == 0 ? a.q : a.k);
       store4(base + (((size_t)r * a.heads + head) * a.ntok + tok) * a.dh + d, v0, v1, v2, v3);
-    } else if constexpr (KIND == EPI_RES_GATE) {
+    } else if constexpr (KIND == EPI_RES_GATE || KIND == EPI_RES_GATE_MLP) {
       const int r = (int)fdiv((uint32_t)m, a.div_ntok);
       const int slot = r < a.n_slots ? r : r - a.n_slots;
       const float4 g = *(const float4*)(a.table + (size_t)slot * a.ldt + a.gate_off + n);
@@ -406,7 +406,7 @@ static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
   switch (tile) {
 #define SF_TILE_CASE(id, bm, bn, wm, wn)                                                   \
   case id:                                                                                  \
-    hipLaunchKernelGGL((gemm_bf16_sched_kernel<bm, bn, wm, wn, KIND>),                      \
+    launch((gemm_bf16_sched_kernel<bm, bn, wm, wn, KIND>),                      \
                        dim3(((a.N + bn - 1) / bn) * ((a.M + bm - 1) / bm)), dim3(wm * wn * 64), 0, s, a); \
     break;
     SF_GEMM_TILES(SF_TILE_CASE)
@@ -433,7 +433,7 @@ template <EpiKind KIND>
 static hipError_t launch_kind(bool use_bf16, int tile, const GemmArgs& a, hipStream_t s) {
   if (use_bf16) return launch_bf16_tile<KIND>(tile < 0 ? choose_gemm_tile(a.M, a.N, a.K) : tile, a, s);
   dim3 grid((a.N + kFT - 1) / kFT, (a.M + kFT - 1) / kFT);
-  hipLaunchKernelGGL(gemm_f32_kernel<KIND>, grid, dim3(256), 0, s, a);
+  launch(gemm_f32_kernel<KIND>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -443,6 +443,7 @@ hipError_t launch_gemm_tile(bool use_bf16, int tile, EpiKind kind, const GemmArg
     case EPI_RES_GATE: return launch_kind<EPI_RES_GATE>(use_bf16, tile, a, s);
     case EPI_GELU: return launch_kind<EPI_GELU>(use_bf16, tile, a, s);
     case EPI_RES: return launch_kind<EPI_RES>(use_bf16, tile, a, s);
+    case EPI_RES_GATE_MLP: return launch_kind<EPI_RES_GATE_MLP>(use_bf16, tile, a, s);
   }
   return hipErrorInvalidValue;
 }

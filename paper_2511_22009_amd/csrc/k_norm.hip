@@ -134,9 +134,9 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
 hipError_t launch_ln(bool out_bf16, const LnArgs& a, hipStream_t s) {
   const int grid = (a.M + 7) / 8;
   if (out_bf16)
-    hipLaunchKernelGGL(ln_mod_kernel<bf16>, dim3(grid), dim3(256), 0, s, a);
+    launch(ln_mod_kernel<bf16>, dim3(grid), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(ln_mod_kernel<float>, dim3(grid), dim3(256), 0, s, a);
+    launch(ln_mod_kernel<float>, dim3(grid), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -216,7 +216,7 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t s) {
   int grid = (M + 15) / 16;
   if (grid > 512) grid = 512;
   const size_t lds = sizeof(float) * a.P * a.D;
-  hipLaunchKernelGGL(head_kernel, dim3(grid), dim3(256), lds, s, a);
+  launch(head_kernel, dim3(grid), dim3(256), lds, s, a);
   return hipGetLastError();
 }
 

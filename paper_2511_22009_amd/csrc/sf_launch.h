@@ -1,11 +1,28 @@
 // Internal interface between the C-ABI runtime (streamflow.cpp) and the gfx950
 // kernels: argument structs and launchers. Not part of the public ABI.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace sf {
+
+// Events that the next kernel launched from this host thread attaches to its own
+// dispatch packet, so they hold that kernel's start and end timestamps rather than
+// those of the stream around it. launch() consumes them (one kernel only).
+struct LaunchEvents {
+  hipEvent_t start;
+  hipEvent_t stop;
+};
+extern thread_local LaunchEvents t_launch_events;
+
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t s, Args... args) {
+  const LaunchEvents ev = t_launch_events;
+  t_launch_events = LaunchEvents{nullptr, nullptr};
+  hipExtLaunchKernelGGL(kernel, grid, block, lds, s, ev.start, ev.stop, 0u, args...);
+}
 
 constexpr int kMaxRows = 64;     // equals SF_MAX_ROWS
 constexpr int kMaxWidth = 2048;  // largest D / mlp input width a row kernel holds
@@ -91,7 +108,9 @@ enum EpiKind {
   EPI_QKV = 0,       // + bias, scatter to head-major q / k and transposed v
   EPI_RES_GATE = 1,  // h += gate[slot][n] * (acc + bias)
   EPI_GELU = 2,      // out = GELU_tanh(acc + bias)
-  EPI_RES = 3        // h += acc + bias
+  EPI_RES = 3,       // h += acc + bias
+  EPI_RES_GATE_MLP = 4  // EPI_RES_GATE for the MLP down-projection (a separate kernel
+                        // symbol, so profiles tell it from the attention projection)
 };
 struct GemmArgs {
   const void* A;

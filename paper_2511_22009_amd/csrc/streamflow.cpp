@@ -30,6 +30,8 @@ FastDiv make_fastdiv(uint32_t d) {
 
 }  // namespace sf
 
+thread_local sf::LaunchEvents sf::t_launch_events{nullptr, nullptr};
+
 namespace {
 
 constexpr size_t kAlign = 256;
@@ -276,15 +278,26 @@ void fill_weights(sf_model* m, const char* blob, std::vector<char>& img) {
 }
 
 // ------------------------------------------------------------- launch helpers
+// Classes whose launch is one kernel get the events on that kernel's own dispatch
+// (pure kernel time); the others (several kernels) are bracketed on the stream.
+constexpr bool one_kernel_class(int kc) { return kc != SF_KC_TEMB && kc != SF_KC_CROSS; }
+
 template <typename F>
 int timed(sf_model* m, int kc, hipStream_t s, F&& launch) {
   Timing& tm = m->timing[kc];
   const bool rec = tm.on && tm.used < kTimingPool;
-  if (rec && hipEventRecord(tm.ev[2 * tm.used], s) != hipSuccess) return SF_E_HIP;
-  if (launch() != hipSuccess) return SF_E_HIP;
+  hipEvent_t e0 = rec ? tm.ev[2 * tm.used] : nullptr, e1 = rec ? tm.ev[2 * tm.used + 1] : nullptr;
+  const bool attach = rec && one_kernel_class(kc);
+  if (rec && !attach && hipEventRecord(e0, s) != hipSuccess) return SF_E_HIP;
+  if (attach) sf::t_launch_events = sf::LaunchEvents{e0, e1};
+  const hipError_t err = launch();
+  const bool consumed = attach && sf::t_launch_events.start == nullptr;
+  sf::t_launch_events = sf::LaunchEvents{nullptr, nullptr};
+  if (err != hipSuccess) return SF_E_HIP;
   if (tm.on) ++tm.launches;
   if (rec) {
-    if (hipEventRecord(tm.ev[2 * tm.used + 1], s) != hipSuccess) return SF_E_HIP;
+    if (attach && !consumed && hipEventRecord(e0, s) != hipSuccess) return SF_E_HIP;  // nothing launched
+    if ((!attach || !consumed) && hipEventRecord(e1, s) != hipSuccess) return SF_E_HIP;
     ++tm.used;
   }
   return SF_OK;
@@ -430,7 +443,7 @@ int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows
       sf::GemmArgs g = gemm_base(m->f, h.mlp, b.W_fc2, h.mlp, M, D, h.mlp, b.b_fc2);
       g.h = m->h; g.ldh = D; g.table = m->table; g.ldt = m->modw; g.gate_off = base + 5 * D;
       g.n_slots = n_lat; g.div_ntok = div_n;
-      return sf::launch_gemm(m->bf16, sf::EPI_RES_GATE, g, s);
+      return sf::launch_gemm(m->bf16, sf::EPI_RES_GATE_MLP, g, s);
     }));
   }
   if (!head_out) return SF_OK;
