@@ -68,7 +68,7 @@ _LIB = None
 _P = ctypes.c_void_p
 _I = ctypes.c_int
 _SIGS = {
-    "sf_load_weights": (_I, [ctypes.c_char_p, ctypes.c_size_t, _I, _I, ctypes.POINTER(_P)]),
+    "sf_load_weights": (_I, [ctypes.c_void_p, ctypes.c_size_t, _I, _I, ctypes.POINTER(_P)]),
     "sf_free": (None, [_P]),
     "sf_strerror": (ctypes.c_char_p, [_I]),
     "sf_get_info": (_I, [_P, ctypes.POINTER(_Info)]),
@@ -148,10 +148,17 @@ class Cond:
 class Model:
     """A loaded velocity network (weights + workspace on the current HIP device)."""
 
-    def __init__(self, blob: bytes, precision=Precision.BF16, max_rows=8):
+    def __init__(self, blob, precision=Precision.BF16, max_rows=8):
+        """`blob`: the weight blob as bytes or any writable buffer (bytearray, numpy)."""
         L = load_library()
         h = ctypes.c_void_p()
-        _check(L.sf_load_weights(blob, len(blob), int(precision), int(max_rows), ctypes.byref(h)),
+        if isinstance(blob, bytes):
+            ptr, n = ctypes.cast(ctypes.c_char_p(blob), ctypes.c_void_p), len(blob)
+        else:
+            mv = memoryview(blob).cast("B")
+            n = mv.nbytes
+            ptr = ctypes.cast((ctypes.c_char * n).from_buffer(mv), ctypes.c_void_p)
+        _check(L.sf_load_weights(ptr, n, int(precision), int(max_rows), ctypes.byref(h)),
                "sf_load_weights")
         self._h = h
         info = _Info()

@@ -36,7 +36,7 @@ def _load(blob, prec=0, max_rows=4):
 
 @pytest.fixture(scope="module")
 def tiny_blob():
-    return W.make_blob(W.get_config("tiny"))
+    return bytes(W.make_blob(W.get_config("tiny")))
 
 
 def test_load_rejects_bad_arguments(tiny_blob):
@@ -62,9 +62,9 @@ def test_load_rejects_malformed_blobs(tiny_blob):
 def test_load_rejects_unsupported_shapes():
     from dataclasses import replace
     cfg = replace(W.get_config("tiny"), D=132, heads=4)          # head dim 33: not a multiple of 8
-    assert _load(W.make_blob(cfg)) == -6
+    assert _load(bytes(W.make_blob(cfg))) == -6
     cfg = replace(W.get_config("tiny"), D=256, heads=1, mlp=512)  # head dim 256 > 128
-    assert _load(W.make_blob(cfg)) == -6
+    assert _load(bytes(W.make_blob(cfg))) == -6
 
 
 def test_calls_reject_null_handle_and_arguments():

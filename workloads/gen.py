@@ -1,13 +1,19 @@
 """Seeded generators: weights, latents, contexts and timestep schedules.
 
-All draws use numpy's PCG64 `default_rng(seed)`; normals are drawn in float64 and
-cast to fp32. Seeds: 0 weights, 1 initial slot latents, 100+m the fresh noise of
-image m, 2 the conditioning context, 3 the unconditional context, 4 the irregular
-schedule.
+All draws use numpy's PCG64. Weight tensor i (in blob order) comes from its own
+stream `default_rng([seed, i])`, drawn directly in fp32 and scaled in fp32, so the
+tensors of a multi-GB blob are generated in parallel threads. Latents and contexts
+are float64 normals cast to fp32. Seeds: 0 weights, 1 initial slot latents, 100+m
+the fresh noise of image m, 2 the conditioning context, 3 the unconditional context,
+4 the irregular schedule.
 """
+import os
+import struct
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
-from .blob import tensor_specs, write_blob
+from .blob import HEADER_FMT, MAGIC, VERSION, header_fields, tensor_specs, write_blob
 
 SEED_WEIGHTS = 0
 SEED_LATENTS = 1
@@ -33,6 +39,29 @@ def _pos_table(cfg):
     return pe.astype(np.float32)
 
 
+def _std(cfg, name, shape, init):
+    if init == "tsens" and name.split(".")[-1] in ("W_t1", "W_t2", "W_mod", "W_fmod"):
+        return 1.0 / np.sqrt(shape[1])
+    return 0.02
+
+
+def _fill(cfg, specs, outs, seed, init):
+    """Writes tensor i of `specs` into outs[i] (an fp32 array of its shape)."""
+    def one(i):
+        name, shape = specs[i]
+        a = outs[i]
+        if name == "pos":
+            a[...] = _pos_table(cfg) if init != "zero" else 0.0
+        elif init == "zero":
+            a[...] = 0.0
+        else:
+            np.random.default_rng([seed, i]).standard_normal(out=a, dtype=np.float32)
+            a *= np.float32(_std(cfg, name, shape, init))
+    order = sorted(range(len(specs)), key=lambda i: -int(np.prod(specs[i][1])))
+    with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
+        list(ex.map(one, order))
+
+
 def make_weights(cfg, seed=SEED_WEIGHTS, init=None):
     """Random-init weights for `cfg` as a dict name -> fp32 array.
 
@@ -42,28 +71,32 @@ def make_weights(cfg, seed=SEED_WEIGHTS, init=None):
     init "zero": all zeros (callers then set the tensors they want).
     """
     init = init or cfg.init
-    rng = np.random.default_rng(seed)
-    out = {}
-    for name, shape in tensor_specs(cfg):
-        if name == "pos":
-            out[name] = _pos_table(cfg) if init != "zero" else np.zeros(shape, np.float32)
-            continue
-        if init == "zero":
-            out[name] = np.zeros(shape, np.float32)
-            continue
-        std = 0.02
-        base = name.split(".")[-1]
-        if init == "tsens" and base in ("W_t1", "W_t2", "W_mod", "W_fmod"):
-            std = 1.0 / np.sqrt(shape[1])
-        out[name] = (rng.standard_normal(shape) * std).astype(np.float32)
-    return out
+    specs = tensor_specs(cfg)
+    outs = [np.empty(shape, np.float32) for _, shape in specs]
+    _fill(cfg, specs, outs, seed, init)
+    return {name: a for (name, _), a in zip(specs, outs)}
 
 
 def make_blob(cfg, seed=SEED_WEIGHTS, init=None, tensors=None):
-    """Blob bytes for `cfg` (seeded weights unless `tensors` is given)."""
-    if tensors is None:
-        tensors = make_weights(cfg, seed=seed, init=init)
-    return write_blob(cfg, tensors, seed=seed)
+    """Blob for `cfg` (seeded weights unless `tensors` is given). The seeded blob is
+    generated in place and returned as a uint8 numpy array (no copy of a multi-GB
+    buffer); its bytes equal write_blob(cfg, make_weights(cfg, ...))."""
+    if tensors is not None:
+        return write_blob(cfg, tensors, seed=seed)
+    init = init or cfg.init
+    specs = tensor_specs(cfg)
+    head = struct.pack(HEADER_FMT, MAGIC, VERSION, *header_fields(cfg), seed)
+    total = len(head) + 4 * sum(int(np.prod(shape)) for _, shape in specs)
+    buf = np.empty(total, np.uint8)  # pages are first touched by the fill threads
+    buf[:len(head)] = np.frombuffer(head, np.uint8)
+    outs, off = [], len(head)
+    for _, shape in specs:
+        n = int(np.prod(shape))
+        outs.append(np.frombuffer(buf, dtype="<f4", count=n, offset=off).reshape(shape))
+        off += 4 * n
+    _fill(cfg, specs, outs, seed, init)
+    del outs
+    return buf
 
 
 def latents(cfg, n, seed=SEED_LATENTS):
