@@ -1,35 +1,55 @@
 // K4: softmax attention softmax(q k^T / sqrt(dh)) v for every (network row, head), no
 // mask; each row attends only to its own tokens, so samples never mix.
 //
-// bf16 path (v_mfma_f32_32x32x16_bf16), online softmax over 64-key tiles:
-//   * a workgroup owns 128 queries of one (row, head); each of its 4 wavefronts owns 32;
+// bf16 path (v_mfma_f32_32x32x16_bf16), online softmax:
+//   * a workgroup owns 64 queries of one (row, head) and four wavefronts: two query
+//     groups of 32 times two key halves. Each step stages 64 keys; the first 32 go to
+//     the key-half-0 wavefronts, the next 32 to key-half-1, and the two halves' partial
+//     results (running max, sum, output) are merged at the end. Splitting the keys
+//     inside the workgroup gives 4 wavefronts per 64 queries, so a 512^2 layer (49152
+//     queries) is 768 workgroups, three per CU on 256 CUs;
 //   * scores are computed transposed, S^T = K Q^T, so the MFMA result gives each lane
-//     ONE query (column l%32) and 16 of the 32 keys of a 32-key block: the running max
+//     ONE query (column l%32) and 16 of the 32 keys of the block: the running max
 //     and sum are lane-local plus a single cross-half shuffle;
+//   * the running max is only moved when a block's max exceeds it by more than 2^8 (in
+//     exp2 units), so the rescale of the output accumulators is rare; probabilities
+//     are then at most 256, which bf16 and the fp32 sums carry exactly as well;
 //   * the probabilities are rounded to bf16 and used directly as the B operand of
 //     O^T = V^T P^T: the MFMA's k-slot order is a permutation of the key order, and V^T
 //     is read from LDS under the same permutation (two 8-byte reads per fragment);
-//   * K and V^T tiles are double-buffered in LDS and fetched one tile ahead through
-//     registers; rows past dh and keys past Nk are zero, so padding adds nothing.
+//   * K and V^T tiles are double-buffered in LDS and fetched one step ahead through
+//     registers with raw buffer loads (keys past the end read as zeros, no branches);
+//     rows past dh and keys past Nk are zero, so padding adds nothing.
 // fp32 path: one thread per query, keys staged in LDS (parity mode).
 #include "sf_device.h"
 
 namespace sf {
 
-constexpr int kBKV = 64;   // keys per tile
-constexpr int kQB = 128;   // queries per workgroup
+constexpr int kKH = 32;    // keys per half per step
+constexpr int kQB = 64;    // queries per workgroup
+constexpr float kLazy = 8.0f;  // max drift (exp2 units) tolerated before a rescale
 
 template <int DHC, int DB>  // DHC = ceil(dh/16) contraction chunks, DB = ceil(dh/32) dh blocks
 __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   constexpr int KLD = DHC * 16 + 8;     // K tile row pitch (bf16)
-  constexpr int VLD = kBKV + 8;         // V^T tile row pitch (bf16)
+  constexpr int VLD = kKH + 8;          // V^T tile row pitch (bf16)
   constexpr int VROWS = DB * 32;
-  constexpr int KCH = (kBKV * DHC * 2 + 255) / 256;   // 16-byte K chunks per thread (upper bound)
-  constexpr int VCH = (VROWS * (kBKV / 8) + 255) / 256;
-  __shared__ bf16 Ks[2][kBKV * KLD];
-  __shared__ bf16 Vs[2][VROWS * VLD];
+  constexpr int KT = kKH * KLD;         // one half's K tile (bf16 elements)
+  constexpr int VT = VROWS * VLD;       // one half's V^T tile
+  constexpr int KCHMAX = 2 * kKH * DHC * 2;        // 16-byte K chunks per step (upper bound)
+  constexpr int VCHMAX = VROWS * (2 * kKH / 8);    // 16-byte V^T chunks per step (upper bound)
+  constexpr int KCH = (KCHMAX + 255) / 256;
+  constexpr int VCH = (VCHMAX + 255) / 256;
+  constexpr int TILE_BYTES = 2 * 2 * (KT + VT) * 2;             // [buf][half] K and V^T
+  constexpr int MERGE_BYTES = 2 * 64 * (DB * 16 + 2) * 4;       // per query group: o, m, l
+  constexpr int SMEM = (TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) + 16;  // + spare slot
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  bf16* const Ks = (bf16*)smem;                  // [buf][half][kKH][KLD]
+  bf16* const Vs = Ks + 2 * 2 * KT;              // [buf][half][VROWS][VLD]
+  const int SPARE = (TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) / 2;  // bf16 index
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int qg = wave & 1, kh = wave >> 1;
   const int l32 = lane & 31, g = lane >> 5;
   // Workgroup b runs on XCD b % 8. Give each XCD a contiguous range of (row, head,
   // query block) triples, query blocks fastest, so the query blocks that stream the same
@@ -47,63 +67,63 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const bf16* Q = (const bf16*)a.q + bh * a.Nq * dh;
   const bf16* Kg = (const bf16*)a.k + bh * a.Nk * dh;
   const bf16* Vt = (const bf16*)a.vT + bh * dh * a.ldv;
-  const int qi = qblk * kQB + wave * 32 + l32;
+  const int qi = qblk * kQB + qg * 32 + l32;
 
-  // zero both buffers once: padding columns/rows are never written by the staging
-  for (int i = tid; i < 2 * kBKV * KLD; i += 256) (&Ks[0][0])[i] = (bf16)0.0f;
-  for (int i = tid; i < 2 * VROWS * VLD; i += 256) (&Vs[0][0])[i] = (bf16)0.0f;
+  // zero the tile buffers once: padding columns (dh..KLD) and rows (dh..VROWS) are
+  // never written by the staging
+  for (int i = tid; i < TILE_BYTES / 16; i += 256) ((u32x4*)smem)[i] = u32x4{0u, 0u, 0u, 0u};
 
   bf16x8 qf[DHC];
+  const __amdgpu_buffer_rsrc_t q_src = buffer_rsrc(Q, (uint32_t)a.Nq * dh * 2);
 #pragma unroll
   for (int kk = 0; kk < DHC; ++kk) {
     const int d0 = kk * 16 + g * 8;
-    if (qi < a.Nq && d0 < dh) {
-      qf[kk] = *(const bf16x8*)(Q + (size_t)qi * dh + d0);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qf[kk][e] = (bf16)0.0f;
-    }
+    const u32x4 w = buffer_load16(q_src, (qi < a.Nq && d0 < dh) ? (qi * dh + d0) * 2 : kOffOOB);
+    qf[kk] = __builtin_bit_cast(bf16x8, w);
   }
 
-  const int kchunks = kBKV * (dh >> 3);       // K tile: kBKV rows x dh/8 chunks
-  const int vchunks = dh * (kBKV / 8);        // V^T tile: dh rows x 8 chunks
-  // K and V^T come in through raw buffer loads: keys past Nk (K) and columns past the
-  // padded row (V^T) get an out-of-range offset and read as zeros, without branches.
+  // staging map, fixed per thread: K chunk c = (key 0..63, 16-byte column); V^T chunk
+  // c = (dh row, 8-key column group 0..7). Chunks past the real count read zeros and
+  // land in the spare slot.
+  const int dh8 = dh >> 3;
+  const int kchunks = 2 * kKH * dh8;
+  const int vchunks = dh * (2 * kKH / 8);
   const __amdgpu_buffer_rsrc_t k_src = buffer_rsrc(Kg, (uint32_t)a.Nk * dh * 2);
   const __amdgpu_buffer_rsrc_t v_src = buffer_rsrc(Vt, (uint32_t)dh * a.ldv * 2);
-  int k_row[KCH], k_col[KCH], v_off[VCH], v_kv[VCH];
+  int k_key[KCH], k_goff[KCH], k_lds[KCH], v_key[VCH], v_goff[VCH], v_lds[VCH];
 #pragma unroll
   for (int i = 0; i < KCH; ++i) {
     const int c = tid + i * 256;
-    k_row[i] = c < kchunks ? c / (dh >> 3) : 1 << 20;
-    k_col[i] = c < kchunks ? (c - (c / (dh >> 3)) * (dh >> 3)) * 8 : 0;
+    const bool in = c < kchunks;
+    const int key = in ? c / dh8 : 0, col = in ? (c - key * dh8) * 8 : 0;
+    k_key[i] = in ? key : 1 << 24;
+    k_goff[i] = (key * dh + col) * 2;
+    k_lds[i] = in ? (key >> 5) * KT + (key & 31) * KLD + col : -1;
   }
 #pragma unroll
   for (int i = 0; i < VCH; ++i) {
     const int c = tid + i * 256;
-    v_kv[i] = (c & 7) * 8;
-    v_off[i] = c < vchunks ? ((c >> 3) * a.ldv + v_kv[i]) * 2 : kOffOOB;
+    const bool in = c < vchunks;
+    const int d = in ? c >> 3 : 0, kg = c & 7;
+    v_key[i] = in ? kg * 8 : 1 << 24;
+    v_goff[i] = (d * a.ldv + kg * 8) * 2;
+    v_lds[i] = in ? (kg >> 2) * VT + d * VLD + (kg & 3) * 8 : -1;
   }
   u32x4 rk[KCH], rv[VCH];
   auto gload = [&](int kv0) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int row = kv0 + k_row[i];
-      rk[i] = buffer_load16(k_src, row < a.Nk ? (row * dh + k_col[i]) * 2 : kOffOOB);
-    }
+    for (int i = 0; i < KCH; ++i)
+      rk[i] = buffer_load16(k_src, kv0 + k_key[i] < a.Nk ? k_goff[i] + kv0 * dh * 2 : kOffOOB);
 #pragma unroll
     for (int i = 0; i < VCH; ++i)
-      rv[i] = buffer_load16(v_src, (v_off[i] != kOffOOB && kv0 + v_kv[i] < a.ldv) ? v_off[i] + 2 * kv0 : kOffOOB);
+      rv[i] = buffer_load16(v_src, kv0 + v_key[i] < a.ldv ? v_goff[i] + kv0 * 2 : kOffOOB);
   };
   auto lstore = [&](int buf) {
+    // the chunk counts depend on dh at run time, so every chunk checks its slot
 #pragma unroll
-    for (int i = 0; i < KCH; ++i)
-      if (tid + i * 256 < kchunks) *(u32x4*)&Ks[buf][k_row[i] * KLD + k_col[i]] = rk[i];
+    for (int i = 0; i < KCH; ++i) *(u32x4*)&Ks[k_lds[i] >= 0 ? buf * 2 * KT + k_lds[i] : SPARE] = rk[i];
 #pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int c = tid + i * 256;
-      if (c < vchunks) *(u32x4*)&Vs[buf][(c >> 3) * VLD + (c & 7) * 8] = rv[i];
-    }
+    for (int i = 0; i < VCH; ++i) *(u32x4*)&Vs[v_lds[i] >= 0 ? buf * 2 * VT + v_lds[i] : SPARE - 4 * KT] = rv[i];
   };
 
   f32x16 o[DB];
@@ -111,67 +131,56 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   for (int b = 0; b < DB; ++b)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[b][e] = 0.0f;
-  float mrow = -INFINITY, lsum = 0.0f;
-  const float sl2 = a.scale * 1.4426950408889634f;  // scores in log2 units
+  float m2 = -INFINITY, lsum = 0.0f;               // running max in exp2 units, partial sum
+  const float sl2 = a.scale * 1.4426950408889634f;  // scores -> exp2 units
 
-  const int ntiles = (a.Nk + kBKV - 1) / kBKV;
+  const int nsteps = (a.Nk + 2 * kKH - 1) / (2 * kKH);
   __syncthreads();
   gload(0);
   lstore(0);
   __syncthreads();
-  for (int it = 0; it < ntiles; ++it) {
+  for (int it = 0; it < nsteps; ++it) {
     const int cur = it & 1;
-    const int kv0 = it * kBKV;
-    if (it + 1 < ntiles) gload(kv0 + kBKV);
+    const int kv0 = it * 2 * kKH + kh * kKH;      // this wavefront's first key
+    if (it + 1 < nsteps) gload((it + 1) * 2 * kKH);
+    const bf16* Kb = Ks + (cur * 2 + kh) * KT;
+    const bf16* Vb = Vs + (cur * 2 + kh) * VT;
 
-    f32x16 s[2];
+    f32x16 s;
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
+    for (int e = 0; e < 16; ++e) s[e] = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) s[c][e] = 0.0f;
-#pragma unroll
-      for (int kk = 0; kk < DHC; ++kk) {
-        const bf16x8 kf = *(const bf16x8*)&Ks[cur][(c * 32 + l32) * KLD + kk * 16 + g * 8];
-        s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[c], 0, 0, 0);
-      }
+    for (int kk = 0; kk < DHC; ++kk) {
+      const bf16x8 kf = *(const bf16x8*)&Kb[l32 * KLD + kk * 16 + g * 8];
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
     }
-    // s[c][e]: query l32, key kv0 + c*32 + (e/4)*8 + g*4 + e%4. Raw scores; the
-    // scale (log2 e / sqrt(dh)) is folded into the exp2 argument. Only the last,
-    // ragged tile needs the key mask.
-    if (kv0 + kBKV > a.Nk) {
+    // s[e]: query l32, key kv0 + (e/4)*8 + g*4 + e%4, raw (unscaled). Only the last,
+    // ragged step needs the key mask.
+    if (kv0 + kKH > a.Nk) {
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int kv = kv0 + c * 32 + (e >> 2) * 8 + g * 4 + (e & 3);
-          if (kv >= a.Nk) s[c][e] = -INFINITY;
-        }
+      for (int e = 0; e < 16; ++e)
+        if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) s[e] = -INFINITY;
     }
-    float tmax = s[0][0];
+    float tmax = s[0];
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, s[c][e]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-    const float mnew = fmaxf(mrow, tmax);
-    // rescale the running output and sum only when some query's max moved
-    if (__any(mnew != mrow)) {
-      const float alpha = __builtin_amdgcn_exp2f((mrow - mnew) * sl2);
+    for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, s[e]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+    if (__any(tmax > m2 + kLazy)) {
+      const float mnew = fmaxf(m2, tmax);
+      const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
       lsum *= alpha;
 #pragma unroll
       for (int b = 0; b < DB; ++b)
 #pragma unroll
         for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
+      m2 = mnew;
     }
-    mrow = mnew;
-    const float moff = -mnew * sl2;
-
-    bf16x8 pf[4];
+    bf16x8 pf[2];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[ks >> 1][(ks & 1) * 8 + j], sl2, moff));
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[ks * 8 + j], sl2, -m2));
         lsum += p;
         pf[ks][j] = (bf16)p;
       }
@@ -179,18 +188,35 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int b = 0; b < DB; ++b) {
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const bf16* vr = &Vs[cur][(b * 32 + l32) * VLD + ks * 16 + g * 4];
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16* vr = &Vb[(b * 32 + l32) * VLD + ks * 16 + g * 4];
         const bf16x4 lo = *(const bf16x4*)vr;
         const bf16x4 hi = *(const bf16x4*)(vr + 8);
         const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
       }
     }
-    if (it + 1 < ntiles) lstore(cur ^ 1);
+    if (it + 1 < nsteps) lstore(cur ^ 1);
     __syncthreads();
   }
 
+  // merge the key halves: half 1 hands (o, max, partial sum) to half 0 through LDS
+  float* mg = (float*)smem + qg * 64 * (DB * 16 + 2);
+  if (kh == 1) {
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mg[(b * 16 + e) * 64 + lane] = o[b][e];
+    mg[DB * 16 * 64 + lane] = m2;
+    mg[(DB * 16 + 1) * 64 + lane] = lsum;
+  }
+  __syncthreads();
+  if (kh == 1) return;
+  const float m2b = mg[DB * 16 * 64 + lane];
+  const float mnew = fmaxf(m2, m2b);
+  const float a0 = m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2 - mnew);
+  const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
+  lsum = lsum * a0 + mg[(DB * 16 + 1) * 64 + lane] * a1;
   lsum += __shfl_xor(lsum, 32);
   const float inv = 1.0f / lsum;
   if (qi < a.Nq) {
@@ -200,11 +226,13 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int e4 = 0; e4 < 4; ++e4) {
         const int d = b * 32 + e4 * 8 + g * 4;
-        if (d < dh) {
-          const bf16x4 w = {(bf16)(o[b][e4 * 4 + 0] * inv), (bf16)(o[b][e4 * 4 + 1] * inv),
-                            (bf16)(o[b][e4 * 4 + 2] * inv), (bf16)(o[b][e4 * 4 + 3] * inv)};
-          *(bf16x4*)(O + d) = w;
+        float w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int e = e4 * 4 + q;
+          w[q] = (o[b][e] * a0 + mg[(b * 16 + e) * 64 + lane] * a1) * inv;
         }
+        if (d < dh) *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
       }
   }
 }

@@ -84,60 +84,111 @@ __device__ __forceinline__ void ln_store_row(const LnArgs& a, int m, int lane, c
   }
 }
 
-// Two rows per wavefront, both rows' loads issued before either reduction.
-template <typename OT>
+// RPW rows per wavefront, NV float4 per lane per row (D <= 256 NV). Every load of
+// the wavefront's rows and of their table entries (shift and scale) is issued before
+// the first reduction, so the kernel pays one memory latency per row group.
+template <typename OT, int NV, int RPW>
 __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
   const int lane = threadIdx.x & 63;
-  const int m0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * 2;
-  if (m0 >= a.M) return;
-  const int m1 = min(m0 + 1, a.M - 1);
+  const int mb = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW;
+  if (mb >= a.M) return;
   const int nv = a.D >> 2;
-  float4 v0[kLnVec], v1[kLnVec];
-  const float4* r0 = (const float4*)(a.h + (size_t)m0 * a.D);
-  const float4* r1 = (const float4*)(a.h + (size_t)m1 * a.D);
+  float4 v[RPW][NV], sc[RPW][NV], sh[RPW][NV];
 #pragma unroll
-  for (int i = 0; i < kLnVec; ++i) {
-    const int c = lane + i * 64;
-    if (c < nv) {
-      v0[i] = r0[c];
-      v1[i] = r1[c];
+  for (int r = 0; r < RPW; ++r) {
+    const int m = min(mb + r, a.M - 1);
+    const float4* row = (const float4*)(a.h + (size_t)m * a.D);
+    const float* tsh = nullptr;
+    const float* tsc = nullptr;
+    if (a.table) {
+      const int q = (int)fdiv((uint32_t)m, a.tok);
+      const int slot = q < a.n_slots ? q : q - a.n_slots;
+      tsh = a.table + (size_t)slot * a.ldt + a.shift_off;
+      tsc = a.table + (size_t)slot * a.ldt + a.scale_off;
+    }
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane + i * 64;
+      const bool in = c < nv;
+      v[r][i] = in ? row[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      if (a.table && in) {
+        sc[r][i] = *(const float4*)(tsc + 4 * c);
+        sh[r][i] = *(const float4*)(tsh + 4 * c);
+      } else {
+        sc[r][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        sh[r][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
     }
   }
-  float s0 = 0.0f, s1 = 0.0f;
+  float mean[RPW], rstd[RPW];
 #pragma unroll
-  for (int i = 0; i < kLnVec; ++i) {
-    const int c = lane + i * 64;
-    if (c < nv) {
-      s0 += (v0[i].x + v0[i].y) + (v0[i].z + v0[i].w);
-      s1 += (v1[i].x + v1[i].y) + (v1[i].z + v1[i].w);
+  for (int r = 0; r < RPW; ++r) {
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) s += (v[r][i].x + v[r][i].y) + (v[r][i].z + v[r][i].w);
+    mean[r] = wave_sum(s) / (float)a.D;
+  }
+#pragma unroll
+  for (int r = 0; r < RPW; ++r) {
+    float q = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      if (lane + i * 64 < nv) {
+        float d;
+        d = v[r][i].x - mean[r]; q += d * d; d = v[r][i].y - mean[r]; q += d * d;
+        d = v[r][i].z - mean[r]; q += d * d; d = v[r][i].w - mean[r]; q += d * d;
+      }
+    }
+    rstd[r] = 1.0f / sqrtf(wave_sum(q) / (float)a.D + kLnEps);
+  }
+#pragma unroll
+  for (int r = 0; r < RPW; ++r) {
+    const int m = mb + r;
+    if (m >= a.M) break;
+    OT* out = (OT*)a.out + (size_t)m * a.D;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane + i * 64;
+      if (c < nv) {
+        float y0 = (v[r][i].x - mean[r]) * rstd[r], y1 = (v[r][i].y - mean[r]) * rstd[r];
+        float y2 = (v[r][i].z - mean[r]) * rstd[r], y3 = (v[r][i].w - mean[r]) * rstd[r];
+        if (a.table) {
+          y0 = y0 * (1.0f + sc[r][i].x) + sh[r][i].x;
+          y1 = y1 * (1.0f + sc[r][i].y) + sh[r][i].y;
+          y2 = y2 * (1.0f + sc[r][i].z) + sh[r][i].z;
+          y3 = y3 * (1.0f + sc[r][i].w) + sh[r][i].w;
+        }
+        Store4<OT>::run(out + 4 * c, y0, y1, y2, y3);
+      }
     }
   }
-  const float mean0 = wave_sum(s0) / (float)a.D, mean1 = wave_sum(s1) / (float)a.D;
-  float q0 = 0.0f, q1 = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kLnVec; ++i) {
-    const int c = lane + i * 64;
-    if (c < nv) {
-      float d;
-      d = v0[i].x - mean0; q0 += d * d; d = v0[i].y - mean0; q0 += d * d;
-      d = v0[i].z - mean0; q0 += d * d; d = v0[i].w - mean0; q0 += d * d;
-      d = v1[i].x - mean1; q1 += d * d; d = v1[i].y - mean1; q1 += d * d;
-      d = v1[i].z - mean1; q1 += d * d; d = v1[i].w - mean1; q1 += d * d;
-    }
+}
+
+template <typename OT, int NV>
+static void launch_ln_nv(const LnArgs& a, hipStream_t s) {
+  constexpr int RPW = NV <= 4 ? 2 : 1;
+  const int grid = (a.M + 4 * RPW - 1) / (4 * RPW);
+  launch((ln_mod_kernel<OT, NV, RPW>), dim3(grid), dim3(256), 0, s, a);
+}
+
+template <typename OT>
+static hipError_t launch_ln_t(const LnArgs& a, hipStream_t s) {
+  switch ((a.D + 255) / 256) {
+    case 1: launch_ln_nv<OT, 1>(a, s); break;
+    case 2: launch_ln_nv<OT, 2>(a, s); break;
+    case 3: launch_ln_nv<OT, 3>(a, s); break;
+    case 4: launch_ln_nv<OT, 4>(a, s); break;
+    case 5: launch_ln_nv<OT, 5>(a, s); break;
+    case 6: launch_ln_nv<OT, 6>(a, s); break;
+    case 7: launch_ln_nv<OT, 7>(a, s); break;
+    case 8: launch_ln_nv<OT, 8>(a, s); break;
+    default: return hipErrorInvalidValue;
   }
-  const float rstd0 = 1.0f / sqrtf(wave_sum(q0) / (float)a.D + kLnEps);
-  const float rstd1 = 1.0f / sqrtf(wave_sum(q1) / (float)a.D + kLnEps);
-  ln_store_row<OT>(a, m0, lane, v0, mean0, rstd0);
-  if (m0 + 1 < a.M) ln_store_row<OT>(a, m1, lane, v1, mean1, rstd1);
+  return hipGetLastError();
 }
 
 hipError_t launch_ln(bool out_bf16, const LnArgs& a, hipStream_t s) {
-  const int grid = (a.M + 7) / 8;
-  if (out_bf16)
-    launch(ln_mod_kernel<bf16>, dim3(grid), dim3(256), 0, s, a);
-  else
-    launch(ln_mod_kernel<float>, dim3(grid), dim3(256), 0, s, a);
-  return hipGetLastError();
+  return out_bf16 ? launch_ln_t<bf16>(a, s) : launch_ln_t<float>(a, s);
 }
 
 // W_f lives in LDS for the whole workgroup (staged with independent 16-byte loads);

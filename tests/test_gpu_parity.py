@@ -135,7 +135,7 @@ def test_stream_step_parity(name, prec):
 # -------------------------------------------------------- method invariants on GPU
 
 @pytest.mark.parametrize("prec", PRECS)
-@pytest.mark.parametrize("name", ["tiny_tsens", "ragged"])
+@pytest.mark.parametrize("name", ["tiny_tsens", "ragged", "dh72"])
 def test_heterogeneous_batch_equals_each_sample_alone(name, prec):
     cfg, x, t, _ = _inputs(name)
     m = model(name, prec)
@@ -143,6 +143,18 @@ def test_heterogeneous_batch_equals_each_sample_alone(name, prec):
     for k in range(cfg.K):
         alone = host(m.velocity(dev(x[k:k + 1]), t[k:k + 1]))[0]
         np.testing.assert_array_equal(full[k], alone)
+
+
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("name", SMALL)
+def test_repeated_calls_are_bit_identical(name, prec):
+    """No kernel depends on scheduling: the same call twice gives the same bits."""
+    cfg, x, t, _ = _inputs(name)
+    m = model(name, prec)
+    xd = dev(x)
+    first = host(m.velocity(xd, t))
+    for _ in range(3):
+        np.testing.assert_array_equal(host(m.velocity(xd, t)), first)
 
 
 @pytest.mark.parametrize("prec", PRECS)
