@@ -12,140 +12,132 @@ namespace sf {
 
 constexpr int kGemvSamples = 4;  // samples per pass (inputs held in registers)
 
-template <typename WT>
-__device__ __forceinline__ void load4(const WT* p, float* w);
-
-template <>
-__device__ __forceinline__ void load4<float>(const float* p, float* w) {
-  float4 v = *(const float4*)p;
-  w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
-}
-
-template <>
-__device__ __forceinline__ void load4<bf16>(const bf16* p, float* w) {
-  bf16x4 v = *(const bf16x4*)p;
-  w[0] = (float)v[0]; w[1] = (float)v[1]; w[2] = (float)v[2]; w[3] = (float)v[3];
-}
-
-// Lane `lane` owns elements 4*(lane + 64 c) .. +3 of the input width for c < NCH, so its
-// slice of every sample's input vector stays in registers for all rows; a wavefront
-// streams kGemvRows weight rows at a time (independent loads in flight) and reduces
-// each row's partial sums across the 64 lanes at the end.
-template <typename WT, int NCH, int kGemvRows>
+// Batched GEMV. Each wavefront takes RW consecutive weight rows and reads them with
+// 16-byte buffer loads (lane l holds 16-byte chunks l + 64 c of every row; chunks past
+// the row read as zeros), so all RW * NC loads of a lane are in flight at once and no
+// load sits behind a branch. Four samples' input slices stay in registers (read from
+// X, or built as the sinusoids of 1000 t). The RW x 4 row/sample partial sums leave
+// through butterfly reductions of 16 values. One task (RW rows) per wavefront.
+template <typename WT, int NC, int RW, int XMODE>
 __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
+  constexpr int E = 16 / sizeof(WT);  // elements per 16-byte chunk
+  static_assert(RW * kGemvSamples % 16 == 0, "rows x samples must fill butterfly groups");
   const int lane = threadIdx.x & 63;
-  const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int nw = gridDim.x * 4;
-  const WT* W = (const WT*)a.W;
+  const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RW;
+  if (j0 >= a.R) return;
+  const int nchunk = a.K / E;
+  const __amdgpu_buffer_rsrc_t w_src = buffer_rsrc(a.W, (uint32_t)((size_t)a.R * a.K * sizeof(WT)));
+  const __amdgpu_buffer_rsrc_t x_src = buffer_rsrc(a.X, a.X ? (uint32_t)((size_t)a.B * a.ldx * 4) : 0u);
   for (int b0 = 0; b0 < a.B; b0 += kGemvSamples) {
     const int nb = min(kGemvSamples, a.B - b0);
-    float x[kGemvSamples][NCH][4];
+    u32x4 w[RW][NC];
+#pragma unroll
+    for (int rr = 0; rr < RW; ++rr) {
+      const int j = min(j0 + rr, a.R - 1);
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int ch = lane + 64 * c;
+        w[rr][c] = buffer_load16(w_src, ch < nchunk ? (int)(((uint32_t)j * a.K + ch * E) * sizeof(WT)) : kOffOOB);
+      }
+    }
+    float x[kGemvSamples][NC][E];
 #pragma unroll
     for (int bb = 0; bb < kGemvSamples; ++bb)
 #pragma unroll
-      for (int c = 0; c < NCH; ++c)
+      for (int c = 0; c < NC; ++c) {
+        const int ch = lane + 64 * c;
+        const bool in = bb < nb && ch < nchunk;
+        if constexpr (XMODE == 1) {
+          const int half = a.K >> 1;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int k = 4 * (lane + 64 * c) + e;
-          float v = 0.0f;
-          if (bb < nb && k < a.K) {
-            if (a.x_mode == 1) {
-              const int half = a.K >> 1;
-              const int f = k < half ? k : k - half;
-              const float tau = 1000.0f * a.t.v[b0 + bb];
-              const float phi = tau * a.freqs[f];
-              v = k < half ? cosf(phi) : sinf(phi);
-            } else {
-              v = a.X[(size_t)(b0 + bb) * a.ldx + k];
-            }
+          for (int e = 0; e < E; ++e) {
+            const int k = ch * E + e;
+            const int f = k < half ? k : k - half;
+            const float phi = (1000.0f * a.t.v[b0 + min(bb, nb - 1)]) * a.freqs[in ? f : 0];
+            x[bb][c][e] = in ? (k < half ? cosf(phi) : sinf(phi)) : 0.0f;
           }
-          x[bb][c][e] = v;
-        }
-    for (int j0 = gw * kGemvRows; j0 < a.R; j0 += nw * kGemvRows) {
-      float acc[kGemvRows][kGemvSamples];
+        } else {
 #pragma unroll
-      for (int rr = 0; rr < kGemvRows; ++rr)
-#pragma unroll
-        for (int bb = 0; bb < kGemvSamples; ++bb) acc[rr][bb] = 0.0f;
-#pragma unroll
-      for (int rr = 0; rr < kGemvRows; ++rr) {
-        const int j = min(j0 + rr, a.R - 1);
-        const WT* wr = W + (size_t)j * a.K;
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          const int k = 4 * (lane + 64 * c);
-          if (k < a.K) {
-            float w[4];
-            load4<WT>(wr + k, w);
-            // explicit fma chain: every sample slot runs the same operation sequence, so
-            // a sample's result does not depend on which slot of the batch it sits in
-#pragma unroll
-            for (int bb = 0; bb < kGemvSamples; ++bb) {
-              float t = acc[rr][bb];
-              t = fmaf(w[0], x[bb][c][0], t);
-              t = fmaf(w[1], x[bb][c][1], t);
-              t = fmaf(w[2], x[bb][c][2], t);
-              t = fmaf(w[3], x[bb][c][3], t);
-              acc[rr][bb] = t;
-            }
+          for (int q = 0; q < E / 4; ++q) {
+            const u32x4 v = buffer_load16(x_src, in ? ((b0 + bb) * a.ldx + ch * E + 4 * q) * 4 : kOffOOB);
+            const float4 f = __builtin_bit_cast(float4, v);
+            x[bb][c][4 * q + 0] = f.x; x[bb][c][4 * q + 1] = f.y;
+            x[bb][c][4 * q + 2] = f.z; x[bb][c][4 * q + 3] = f.w;
           }
         }
       }
-      if constexpr (kGemvRows * kGemvSamples == 16) {
-        float v16[16];
+    float acc[RW][kGemvSamples];
 #pragma unroll
-        for (int rr = 0; rr < kGemvRows; ++rr)
+    for (int rr = 0; rr < RW; ++rr) {
 #pragma unroll
-          for (int bb = 0; bb < kGemvSamples; ++bb) v16[rr * kGemvSamples + bb] = acc[rr][bb];
-        float sum = wave_reduce16(v16);
-        const int idx = (lane >> 2) & 15;
-        const int rr = idx / kGemvSamples, bb = idx % kGemvSamples;
-        const int j = j0 + rr;
-        if ((lane & 3) == 0 && bb < nb && j < a.R) {
-          sum += a.bias[j];
-          if (a.act == 1) sum = silu(sum);
-          a.Y[(size_t)(b0 + bb) * a.ldy + j] = sum;
+      for (int bb = 0; bb < kGemvSamples; ++bb) acc[rr][bb] = 0.0f;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        float wf[E];
+        if constexpr (E == 8) {
+          const bf16x8 v = __builtin_bit_cast(bf16x8, w[rr][c]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) wf[e] = (float)v[e];
+        } else {
+          const float4 v = __builtin_bit_cast(float4, w[rr][c]);
+          wf[0] = v.x; wf[1] = v.y; wf[2] = v.z; wf[3] = v.w;
         }
-      } else {
+        // the same fma sequence for every sample slot, so a sample's result does not
+        // depend on its slot in the batch
 #pragma unroll
-        for (int rr = 0; rr < kGemvRows; ++rr)
+        for (int bb = 0; bb < kGemvSamples; ++bb) {
+          float t = acc[rr][bb];
 #pragma unroll
-          for (int bb = 0; bb < kGemvSamples; ++bb) {
-            if (bb >= nb) continue;
-            float sum = wave_sum(acc[rr][bb]);
-            const int j = j0 + rr;
-            if (lane == 0 && j < a.R) {
-              sum += a.bias[j];
-              if (a.act == 1) sum = silu(sum);
-              a.Y[(size_t)(b0 + bb) * a.ldy + j] = sum;
-            }
-          }
+          for (int e = 0; e < E; ++e) t = fmaf(wf[e], x[bb][c][e], t);
+          acc[rr][bb] = t;
+        }
+      }
+    }
+#pragma unroll
+    for (int grp = 0; grp < RW * kGemvSamples / 16; ++grp) {
+      constexpr int RG = 16 / kGemvSamples;  // rows per butterfly group
+      float v16[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) v16[q] = acc[grp * RG + q / kGemvSamples][q % kGemvSamples];
+      float sum = wave_reduce16(v16);
+      const int idx = (lane >> 2) & 15;
+      const int rr = grp * RG + idx / kGemvSamples, bb = idx % kGemvSamples;
+      const int j = j0 + rr;
+      if ((lane & 3) == 0 && bb < nb && j < a.R) {
+        sum += a.bias[j];
+        if (a.act == 1) sum = silu(sum);
+        a.Y[(size_t)(b0 + bb) * a.ldy + j] = sum;
       }
     }
   }
 }
 
-template <typename WT, int ROWS>
-static hipError_t launch_gemv_rows(const GemvArgs& a, hipStream_t s) {
-  const int nch = (a.K + 255) / 256;
-  int grid = (a.R + 4 * ROWS - 1) / (4 * ROWS);
-  if (grid > 2048) grid = 2048;
-  switch (nch) {
-#define SF_GEMV_CASE(n) \
-  case n: launch((gemv_kernel<WT, n, ROWS>), dim3(grid), dim3(256), 0, s, a); break;
-    SF_GEMV_CASE(1) SF_GEMV_CASE(2) SF_GEMV_CASE(3) SF_GEMV_CASE(4) SF_GEMV_CASE(5)
-    SF_GEMV_CASE(6) SF_GEMV_CASE(7) SF_GEMV_CASE(8)
-#undef SF_GEMV_CASE
+template <typename WT, int NC>
+static void launch_gemv_nc(const GemvArgs& a, hipStream_t s) {
+  constexpr int RW = NC <= 2 ? 8 : 4;  // keep the loads of a task within the register file
+  const int tasks = (a.R + RW - 1) / RW;
+  if (a.x_mode == 1)
+    launch((gemv_kernel<WT, NC, RW, 1>), dim3((tasks + 3) / 4), dim3(256), 0, s, a);
+  else
+    launch((gemv_kernel<WT, NC, RW, 0>), dim3((tasks + 3) / 4), dim3(256), 0, s, a);
+}
+
+template <typename WT>
+static hipError_t launch_gemv_t(const GemvArgs& a, hipStream_t s) {
+  constexpr int E = 16 / sizeof(WT);
+  if (a.K % E || (size_t)a.R * a.K * sizeof(WT) >= (1ull << 31)) return hipErrorInvalidValue;
+  switch ((a.K / E + 63) / 64) {
+    case 1: launch_gemv_nc<WT, 1>(a, s); break;
+    case 2: launch_gemv_nc<WT, 2>(a, s); break;
+    case 3: launch_gemv_nc<WT, 3>(a, s); break;
+    case 4: launch_gemv_nc<WT, 4>(a, s); break;
+    case 5: launch_gemv_nc<WT, 5>(a, s); break;
+    case 6: launch_gemv_nc<WT, 6>(a, s); break;
+    case 7: launch_gemv_nc<WT, 7>(a, s); break;
+    case 8: launch_gemv_nc<WT, 8>(a, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
-}
-
-// Few rows (the timestep MLP): one row per wavefront for parallelism. Many rows (the
-// adaLN table): four rows per wavefront and one butterfly reduction per row group.
-template <typename WT>
-static hipError_t launch_gemv_t(const GemvArgs& a, hipStream_t s) {
-  return a.R < 16384 ? launch_gemv_rows<WT, 1>(a, s) : launch_gemv_rows<WT, 4>(a, s);
 }
 
 hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s) {
