@@ -146,7 +146,42 @@ hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s) {
 
 // One thread per four consecutive outputs of one token: the token's p*p*C patch values
 // (feature (i*p + j)*C + c of token gh*(W/p) + gw reads x[c][gh*p + i][gw*p + j]) times
-// the transposed patch-embedding weight W_peT [P][D], plus bias and position row.
+// the transposed patch-embedding weight W_peT [P][D], plus bias and position row. The
+// 2x2-patch, 4-channel case has every load unrolled and issued up front (eight 8-byte
+// pixel-pair loads and sixteen weight rows); other shapes take the general loop.
+__global__ __launch_bounds__(256) void embed_p2c4_kernel(EmbedArgs a) {
+  const int d4n = a.D >> 2;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= a.rows * a.N * d4n) return;
+  const int m = idx / d4n, d = (idx - m * d4n) * 4;
+  const int r = m / a.N;
+  const int n = m - r * a.N;
+  const int lat = r % a.n_lat;
+  const int gwn = a.W / 2;
+  const int gh = n / gwn, gw = n - gh * gwn;
+  float px[16];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const float2 v = *(const float2*)(a.x + (((size_t)lat * 4 + c) * a.H + gh * 2 + i) * a.W + gw * 2);
+      px[(2 * i + 0) * 4 + c] = v.x;
+      px[(2 * i + 1) * 4 + c] = v.y;
+    }
+  float4 w[16];
+#pragma unroll
+  for (int f = 0; f < 16; ++f) w[f] = *(const float4*)(a.W_pe + (size_t)f * a.D + d);
+  const float4 b = *(const float4*)(a.b_pe + d);
+  const float4 ps = *(const float4*)(a.pos + (size_t)n * a.D + d);
+  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+  for (int f = 0; f < 16; ++f) {
+    acc.x += px[f] * w[f].x; acc.y += px[f] * w[f].y; acc.z += px[f] * w[f].z; acc.w += px[f] * w[f].w;
+  }
+  *(float4*)(a.h + (size_t)m * a.D + d) =
+      make_float4((acc.x + b.x) + ps.x, (acc.y + b.y) + ps.y, (acc.z + b.z) + ps.z, (acc.w + b.w) + ps.w);
+}
+
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   const int d4n = a.D >> 2;
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
@@ -174,7 +209,10 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   const int total = a.rows * a.N * (a.D >> 2);
-  launch(embed_kernel, dim3((total + 255) / 256), dim3(256), 0, s, a);
+  if (a.p == 2 && a.C == 4)
+    launch(embed_p2c4_kernel, dim3((total + 255) / 256), dim3(256), 0, s, a);
+  else
+    launch(embed_kernel, dim3((total + 255) / 256), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

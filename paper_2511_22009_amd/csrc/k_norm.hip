@@ -9,36 +9,6 @@
 namespace sf {
 
 constexpr float kLnEps = 1e-6f;
-constexpr int kLnVec = kMaxWidth / 4 / 64;  // float4 per lane for the widest row
-
-// Loads one row (D floats, D % 4 == 0) into per-lane registers and returns mean/rstd.
-__device__ __forceinline__ void row_stats(const float* row, int D, int lane, float4 (&v)[kLnVec],
-                                          float& mean, float& rstd) {
-  const int nv = D >> 2;
-  const float4* r4 = (const float4*)row;
-  float s = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kLnVec; ++i) {
-    const int c = lane + i * 64;
-    if (c < nv) {
-      v[i] = r4[c];
-      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
-    }
-  }
-  mean = wave_sum(s) / (float)D;
-  float ss = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kLnVec; ++i) {
-    const int c = lane + i * 64;
-    if (c < nv) {
-      const float a = v[i].x - mean, b = v[i].y - mean, cc = v[i].z - mean, d = v[i].w - mean;
-      ss += (a * a + b * b) + (cc * cc + d * d);
-    }
-  }
-  const float var = wave_sum(ss) / (float)D;
-  rstd = 1.0f / sqrtf(var + kLnEps);
-}
-
 template <typename OT> struct Store4;
 template <> struct Store4<float> {
   __device__ static void run(float* p, float a, float b, float c, float d) {
@@ -51,38 +21,6 @@ template <> struct Store4<bf16> {
     *(bf16x4*)p = o;
   }
 };
-
-template <typename OT>
-__device__ __forceinline__ void ln_store_row(const LnArgs& a, int m, int lane, const float4 (&v)[kLnVec], float mean,
-                                             float rstd) {
-  const float* sh = nullptr;
-  const float* sc = nullptr;
-  if (a.table) {
-    const int r = (int)fdiv((uint32_t)m, a.tok);
-    const int slot = r < a.n_slots ? r : r - a.n_slots;
-    sh = a.table + (size_t)slot * a.ldt + a.shift_off;
-    sc = a.table + (size_t)slot * a.ldt + a.scale_off;
-  }
-  OT* out = (OT*)a.out + (size_t)m * a.D;
-  const int nv = a.D >> 2;
-#pragma unroll
-  for (int i = 0; i < kLnVec; ++i) {
-    const int c = lane + i * 64;
-    if (c < nv) {
-      float y0 = (v[i].x - mean) * rstd, y1 = (v[i].y - mean) * rstd;
-      float y2 = (v[i].z - mean) * rstd, y3 = (v[i].w - mean) * rstd;
-      if (sc) {
-        const float4 s4 = *(const float4*)(sc + 4 * c);
-        const float4 h4 = *(const float4*)(sh + 4 * c);
-        y0 = y0 * (1.0f + s4.x) + h4.x;
-        y1 = y1 * (1.0f + s4.y) + h4.y;
-        y2 = y2 * (1.0f + s4.z) + h4.z;
-        y3 = y3 * (1.0f + s4.w) + h4.w;
-      }
-      Store4<OT>::run(out + 4 * c, y0, y1, y2, y3);
-    }
-  }
-}
 
 // RPW rows per wavefront, NV float4 per lane per row (D <= 256 NV). Every load of
 // the wavefront's rows and of their table entries (shift and scale) is issued before
@@ -191,83 +129,117 @@ hipError_t launch_ln(bool out_bf16, const LnArgs& a, hipStream_t s) {
   return out_bf16 ? launch_ln_t<bf16>(a, s) : launch_ln_t<float>(a, s);
 }
 
-// W_f lives in LDS for the whole workgroup (staged with independent 16-byte loads);
-// each wavefront walks token rows.
+// Four token rows per wavefront. Every load of the rows and of their final
+// shift/scale entries is issued before the first reduction; the linear map D -> P then
+// runs in groups of four outputs: the lane's slice of four W_f rows (read from L2) is
+// applied to all four rows, and the 16 row x output sums leave through one butterfly
+// reduction. The result is written straight to its unpatchified position.
+template <int NV>
 __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
-  extern __shared__ float wf[];  // [P][D]
-  {
-    const int n4 = (a.P * a.D) >> 2;
-    const float4* src = (const float4*)a.W_f;
-    float4* dst = (float4*)wf;
-    constexpr int kStage = kMaxPatch * kMaxWidth / 4 / 256;
-#pragma unroll
-    for (int k = 0; k < kStage; ++k) {
-      const int i = threadIdx.x + k * 256;
-      if (i < n4) dst[i] = src[i];
-    }
-  }
-  __syncthreads();
+  constexpr int RH = 4;
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
   const int M = a.rows * a.N;
+  const int mb = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RH;
+  if (mb >= M) return;
   const int nv = a.D >> 2;
-  const int gwn = a.W / a.p;
-  for (int m = blockIdx.x * 4 + wave; m < M; m += gridDim.x * 4) {
-    float4 v[kLnVec];
-    float mean, rstd;
-    row_stats(a.h + (size_t)m * a.D, a.D, lane, v, mean, rstd);
-    const int r = (int)fdiv((uint32_t)m, a.tok);
-    const int n = m - r * a.N;
-    const int slot = r < a.n_slots ? r : r - a.n_slots;
-    const float* sh = a.table + (size_t)slot * a.ldt + a.shift_off;
-    const float* sc = a.table + (size_t)slot * a.ldt + a.scale_off;
+  float4 v[RH][NV];
+  {
+    float4 sc[RH][NV], sh[RH][NV];
 #pragma unroll
-    for (int i = 0; i < kLnVec; ++i) {
-      const int c = lane + i * 64;
-      if (c < nv) {
-        const float4 s4 = *(const float4*)(sc + 4 * c);
-        const float4 h4 = *(const float4*)(sh + 4 * c);
-        v[i].x = (v[i].x - mean) * rstd * (1.0f + s4.x) + h4.x;
-        v[i].y = (v[i].y - mean) * rstd * (1.0f + s4.y) + h4.y;
-        v[i].z = (v[i].z - mean) * rstd * (1.0f + s4.z) + h4.z;
-        v[i].w = (v[i].w - mean) * rstd * (1.0f + s4.w) + h4.w;
+    for (int r = 0; r < RH; ++r) {
+      const int m = min(mb + r, M - 1);
+      const float4* row = (const float4*)(a.h + (size_t)m * a.D);
+      const int q = (int)fdiv((uint32_t)m, a.tok);
+      const int slot = q < a.n_slots ? q : q - a.n_slots;
+      const float* tsh = a.table + (size_t)slot * a.ldt + a.shift_off;
+      const float* tsc = a.table + (size_t)slot * a.ldt + a.scale_off;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int c = lane + i * 64;
+        const bool in = c < nv;
+        const int cc = in ? c : 0;
+        v[r][i] = in ? row[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+        sc[r][i] = *(const float4*)(tsc + 4 * cc);
+        sh[r][i] = *(const float4*)(tsh + 4 * cc);
       }
     }
-    const int gh = n / gwn, gw = n - gh * gwn;
-    for (int o0 = 0; o0 < a.P; o0 += 16) {
-      float acc[16];
 #pragma unroll
-      for (int o = 0; o < 16; ++o) {
-        acc[o] = 0.0f;
-        if (o0 + o < a.P) {
-          const float* wr = wf + (o0 + o) * a.D;
+    for (int r = 0; r < RH; ++r) {
+      float s = 0.0f;
 #pragma unroll
-          for (int i = 0; i < kLnVec; ++i) {
-            const int c = lane + i * 64;
-            if (c < nv) {
-              const float4 w4 = *(const float4*)(wr + 4 * c);
-              acc[o] += (v[i].x * w4.x + v[i].y * w4.y) + (v[i].z * w4.z + v[i].w * w4.w);
-            }
-          }
+      for (int i = 0; i < NV; ++i) s += (v[r][i].x + v[r][i].y) + (v[r][i].z + v[r][i].w);
+      const float mean = wave_sum(s) / (float)a.D;
+      float q = 0.0f;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        if (lane + i * 64 < nv) {
+          const float d0 = v[r][i].x - mean, d1 = v[r][i].y - mean, d2 = v[r][i].z - mean, d3 = v[r][i].w - mean;
+          q += (d0 * d0 + d1 * d1) + (d2 * d2 + d3 * d3);
         }
       }
-      const float mine = wave_reduce16(acc);
-      const int f = o0 + ((lane >> 2) & 15);
-      if ((lane & 3) == 0 && f < a.P) {
-        const int c = f % a.C, ij = f / a.C;
-        const int i = ij / a.p, j = ij - i * a.p;
-        a.v[(((size_t)r * a.C + c) * a.H + gh * a.p + i) * a.W + gw * a.p + j] = mine + a.b_f[f];
+      const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)a.D + kLnEps);
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const bool in = lane + i * 64 < nv;
+        v[r][i].x = in ? (v[r][i].x - mean) * rstd * (1.0f + sc[r][i].x) + sh[r][i].x : 0.0f;
+        v[r][i].y = in ? (v[r][i].y - mean) * rstd * (1.0f + sc[r][i].y) + sh[r][i].y : 0.0f;
+        v[r][i].z = in ? (v[r][i].z - mean) * rstd * (1.0f + sc[r][i].z) + sh[r][i].z : 0.0f;
+        v[r][i].w = in ? (v[r][i].w - mean) * rstd * (1.0f + sc[r][i].w) + sh[r][i].w : 0.0f;
       }
+    }
+  }
+  const int gwn = a.W / a.p;
+  for (int o0 = 0; o0 < a.P; o0 += 4) {
+    float4 w[4][NV];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float* wr = a.W_f + (size_t)min(o0 + q, a.P - 1) * a.D;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int c = lane + i * 64;
+        w[q][i] = *(const float4*)(wr + 4 * (c < nv ? c : 0));
+      }
+    }
+    float acc[16];
+#pragma unroll
+    for (int r = 0; r < RH; ++r)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float t = 0.0f;
+#pragma unroll
+        for (int i = 0; i < NV; ++i)
+          t += (v[r][i].x * w[q][i].x + v[r][i].y * w[q][i].y) + (v[r][i].z * w[q][i].z + v[r][i].w * w[q][i].w);
+        acc[r * 4 + q] = t;
+      }
+    const float tot = wave_reduce16(acc);
+    const int idx = (lane >> 2) & 15;
+    const int r = idx >> 2, f = o0 + (idx & 3);
+    const int m = mb + r;
+    if ((lane & 3) == 0 && f < a.P && m < M) {
+      const int row = (int)fdiv((uint32_t)m, a.tok);
+      const int n = m - row * a.N;
+      const int gh = n / gwn, gw = n - gh * gwn;
+      const int c = f % a.C, ij = f / a.C;
+      const int i = ij / a.p, j = ij - i * a.p;
+      a.v[(((size_t)row * a.C + c) * a.H + gh * a.p + i) * a.W + gw * a.p + j] = tot + a.b_f[f];
     }
   }
 }
 
 hipError_t launch_head(const HeadArgs& a, hipStream_t s) {
   const int M = a.rows * a.N;
-  int grid = (M + 15) / 16;
-  if (grid > 512) grid = 512;
-  const size_t lds = sizeof(float) * a.P * a.D;
-  launch(head_kernel, dim3(grid), dim3(256), lds, s, a);
+  const dim3 grid((M + 15) / 16);
+  switch ((a.D + 255) / 256) {
+    case 1: launch(head_kernel<1>, grid, dim3(256), 0, s, a); break;
+    case 2: launch(head_kernel<2>, grid, dim3(256), 0, s, a); break;
+    case 3: launch(head_kernel<3>, grid, dim3(256), 0, s, a); break;
+    case 4: launch(head_kernel<4>, grid, dim3(256), 0, s, a); break;
+    case 5: launch(head_kernel<5>, grid, dim3(256), 0, s, a); break;
+    case 6: launch(head_kernel<6>, grid, dim3(256), 0, s, a); break;
+    case 7: launch(head_kernel<7>, grid, dim3(256), 0, s, a); break;
+    case 8: launch(head_kernel<8>, grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
