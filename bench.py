@@ -7,10 +7,12 @@ network call over every in-flight latent, each latent's Euler update, and the sh
 that admits the next fresh latent (one finished latent leaves per step). Inputs
 (weights, latents, a pool of fresh latents) are resident in HBM before timing.
 
-Prints one JSON line: latent-steps/s (value), images/s, the roofline of the dominant
-kernel class (timed with HIP events on the launch stream during the timed steps),
-the per-class time breakdown, the one-latent-at-a-time rate (no stream batching),
-and the oracle timed on the host cores as a CPU baseline.
+Prints one JSON line: latent-steps/s (value), images/s, the median step, the roofline
+of the dominant kernel class (timed with HIP events attached to its dispatches during
+the timed steps), the per-class time breakdown and the achieved GB/s of the
+memory-bound classes, the Alg. 2 rate over 100 images including the fill phase, the
+one-latent-at-a-time rate (no stream batching), and the oracle timed on the host
+cores as a CPU baseline.
 """
 import argparse
 import json
@@ -37,7 +39,7 @@ MI355X_HBM_GBS = 8000.0
 # only for the kernel sources it was measured on (hash below); otherwise traffic is null.
 KERNEL_SOURCES = ("k_gemm.hip", "sf_device.h", "sf_launch.h")
 TRAFFIC = {
-    ("s512", "bf16", "FC2"): {"bytes": 94497912, "sources": "3f3ea8b56adb86c5",
+    ("s512", "bf16", "FC2"): {"bytes": 94580736, "sources": "0bb1754ec287eb11",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
 }
 
@@ -61,6 +63,22 @@ def class_work(cfg, kc, rows):
         KC.FC1: 2.0 * M * D * F,
         KC.FC2: 2.0 * M * F * D,
         KC.ATTN: 4.0 * rows * N * N * D,
+    }.get(kc)
+
+
+def class_bytes(cfg, kc, es):
+    """Algorithmic HBM bytes of ONE launch of a memory-bound kernel class (read once +
+    write once at the kernel's dtypes); es = bytes per element of bf16/fp32 operands."""
+    from paper_2511_22009_amd import KernelClass as KC
+    R, N, D, E, P = cfg.rows, cfg.N, cfg.D, cfg.C * cfg.H * cfg.W, cfg.patch_dim
+    M, B = R * N, cfg.K
+    modw = cfg.L * 6 * D + 2 * D
+    return {
+        KC.TEMB: cfg.tdim * D * 4 + D * D * 4 + modw * D * es + B * modw * 4,
+        KC.EMBED: B * E * 4 + P * D * 4 + N * D * 4 + M * D * 4,
+        KC.LN: M * D * 4 + M * D * es,
+        KC.HEAD: M * D * 4 + P * D * 4 + R * E * 4,
+        KC.EULER: (B + R + 1) * E * 4 + (B + 1) * E * 4,
     }.get(kc)
 
 
@@ -154,12 +172,16 @@ def main():
 
     # timed region: exactly `steps` steps, events on the dominant class only
     m.timing_enable(dom, True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        marks[i].record(stream)
         step(args.warmup + i)
+    marks[-1].record(stream)
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
+    per_step_ms = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
     dom_ms, dom_n = m.timing_read(dom)
     m.timing_enable(dom, False)
     if not bool(torch.isfinite(x).all()):
@@ -171,12 +193,37 @@ def main():
     avg_launch_s = dom_ms / 1e3 / max(dom_n, 1)
     achieved = work / avg_launch_s / 1e12
     peak = MI355X_PEAK_BF16_TFLOPS if args.precision == "bf16" else MI355X_PEAK_FP32_TFLOPS
+    es = 2 if args.precision == "bf16" else 4
+    mem = {}
+    for kc in KernelClass:
+        b = class_bytes(cfg, kc, es)
+        if b and kc.name in breakdown:
+            us = 1e3 * breakdown[kc.name]["ms_per_step"] / breakdown[kc.name]["launches_per_step"]
+            mem[kc.name] = {"us_per_launch": round(us, 2), "bytes_per_launch": b,
+                            "GBps": round(b / us / 1e3, 1), "frac_of_hbm": round(b / us / 1e3 / MI355X_HBM_GBS, 3)}
     tr = TRAFFIC.get((cfg.name, args.precision, dom.name))
     traffic = tr["bytes"] if tr and tr["sources"] == kernel_sources_hash() else None
     gemm_ms = sum(breakdown[k]["ms_per_step"] for k in ("QKV", "PROJ", "FC1", "FC2") if k in breakdown)
     gemm_tflops = cfg.gemm_flops_per_step() / (gemm_ms / 1e3) / 1e12 if gemm_ms else None
 
     # the same kernels one latent at a time (no stream batching): K network calls per image
+    # Alg. 2 end to end: M = 100 images through the fill phase and the full queue
+    # (M + K - 1 stream steps, host driver included)
+    fill_img_s = None
+    if not args.no_sequential:
+        from paper_2511_22009_amd.pipeline import run_images
+        grid = W.schedule(cfg)
+        ctx_of = None
+        if cond is not None:
+            ctx_of = lambda j: cond.ctx[j % K]  # noqa: E731
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        imgs = run_images(m, grid, 100, lambda j: pool[j % pool.shape[0]], ctx_of,
+                          cond.null_ctx if cond is not None else None, cfg.guidance if cond is not None else None)
+        torch.cuda.synchronize()
+        fill_img_s = len(imgs) / (time.perf_counter() - t2)
+        del imgs
+
     seq_img_s = None
     if not args.no_sequential:
         seq_steps = max(4, args.steps // 10)
@@ -214,6 +261,8 @@ def main():
             "slots": K, "rows": cfg.rows, "tokens": cfg.N, "width": cfg.D, "depth": cfg.L,
         },
         "images_per_s": 1e3 / ms_step,
+        "median_ms_per_step": per_step_ms[len(per_step_ms) // 2],
+        "fill_inclusive_images_per_s_M100": fill_img_s,
         "step_tflops": cfg.flops_per_step() / (ms_step / 1e3) / 1e12,
         "step_frac_of_peak": cfg.flops_per_step() / (ms_step / 1e3) / 1e12 / peak,
         "gemm_tflops": gemm_tflops,
@@ -234,6 +283,7 @@ def main():
             "launches_timed": dom_n,
         },
         "breakdown_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in breakdown.items()},
+        "memory_kernels": mem,
     }
     m.close()
     if args.copy_calibration:
