@@ -116,6 +116,7 @@ def main():
     ap.add_argument("--config", default="s512")
     ap.add_argument("--precision", default="bf16", choices=["bf16", "fp32"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-graph", action="store_true", help="skip the graph-replay measurement")
     ap.add_argument("--no-sequential", action="store_true",
                     help="skip the one-latent-at-a-time comparison run (keeps profiles to the batched step)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -207,6 +208,37 @@ def main():
     gemm_tflops = cfg.gemm_flops_per_step() / (gemm_ms / 1e3) / 1e12 if gemm_ms else None
 
     # the same kernels one latent at a time (no stream batching): K network calls per image
+    # the same steps replayed from captured HIP graphs on a side stream (one graph per
+    # distinct call: the fresh-latent pool has 16 entries, so 16 graphs after warm-up)
+    graph = None
+    if not args.no_graph:
+        gs = torch.cuda.Stream()
+        m.graph_enable(True)
+
+        def gstep(i):
+            m.stream_step(x, t, dt, K, pool[i % pool.shape[0]], done, cond, gs)
+
+        torch.cuda.synchronize()
+        for i in range(pool.shape[0] + max(2, args.warmup)):
+            gstep(i)
+        gmarks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        gs.synchronize()
+        g0 = time.perf_counter()
+        for i in range(args.steps):
+            gmarks[i].record(gs)
+            gstep(i)
+        gmarks[-1].record(gs)
+        gs.synchronize()
+        gel = time.perf_counter() - g0
+        cached, replays = m.graph_stats()
+        m.graph_enable(False)
+        if not bool(torch.isfinite(x).all()):
+            raise RuntimeError("non-finite latents after the graph-replay steps")
+        g_steps = sorted(gmarks[i].elapsed_time(gmarks[i + 1]) for i in range(args.steps))
+        graph = {"ms_per_step": 1e3 * gel / args.steps, "latent_steps_per_s": K / (gel / args.steps),
+                 "median_ms_per_step": g_steps[len(g_steps) // 2], "graphs_cached": cached,
+                 "replays": replays}
+
     # Alg. 2 end to end: M = 100 images through the fill phase and the full queue
     # (M + K - 1 stream steps, host driver included)
     fill_img_s = None
@@ -263,6 +295,7 @@ def main():
         "images_per_s": 1e3 / ms_step,
         "median_ms_per_step": per_step_ms[len(per_step_ms) // 2],
         "fill_inclusive_images_per_s_M100": fill_img_s,
+        "graph_replay": graph,
         "step_tflops": cfg.flops_per_step() / (ms_step / 1e3) / 1e12,
         "step_frac_of_peak": cfg.flops_per_step() / (ms_step / 1e3) / 1e12 / peak,
         "gemm_tflops": gemm_tflops,

@@ -181,6 +181,21 @@ enum {
   SF_KC_COUNT
 };
 
+/* Graph replay of the step (Sec. 3.5 asks for static execution of heterogeneous steps;
+ * here t is data, so one captured launch sequence serves every mix of timesteps).
+ * While enabled, sf_velocity and sf_stream_step capture their launches on the caller's
+ * stream into a HIP graph the first time a given call (entry point, pointers, B, t, dt,
+ * conditioning) is seen, and replay that graph on every identical later call. Up to 64
+ * graphs are kept (least recently used goes first). Requires a non-null stream (the
+ * legacy default stream cannot be captured); on the null stream, or while any kernel
+ * class is being timed, calls run eagerly. Results are bit-identical to eager calls.
+ * Disabling destroys the cached graphs. The captured sequences contain kernel launches
+ * only (no memset or copy nodes). Returns SF_E_HIP if a capture or instantiation fails
+ * (the call's work is then not enqueued). */
+int sf_graph_enable(sf_model* m, int enable);
+/* Number of graphs currently cached and number of replays served from the cache. */
+int sf_graph_stats(const sf_model* m, int* cached, long* replays);
+
 /* Test and bench hook: while enabled, every launch of kernel class `kc` is timed by a
  * pair of HIP events. For a class that is one kernel the events are attached to that
  * kernel's dispatch (its own start and end); SF_KC_TEMB and SF_KC_CROSS, which launch

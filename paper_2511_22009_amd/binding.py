@@ -80,6 +80,8 @@ _SIGS = {
     "sf_debug_read": (_I, [_P, _I, _P, ctypes.c_size_t, _P]),
     "sf_timing_enable": (_I, [_P, _I, _I]),
     "sf_timing_read": (_I, [_P, _I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_long)]),
+    "sf_graph_enable": (_I, [_P, _I]),
+    "sf_graph_stats": (_I, [_P, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_long)]),
 }
 
 
@@ -249,6 +251,16 @@ class Model:
                                             out.numel() * out.element_size(), self._stream(stream)),
                "sf_debug_read")
         return out.float()
+
+    def graph_enable(self, on=True):
+        """Capture each distinct velocity / stream-step call into a HIP graph and replay it
+        on identical calls (needs a non-default stream; see sf_graph_enable)."""
+        _check(load_library().sf_graph_enable(self._h, 1 if on else 0), "sf_graph_enable")
+
+    def graph_stats(self):
+        cached, replays = ctypes.c_int(), ctypes.c_long()
+        _check(load_library().sf_graph_stats(self._h, ctypes.byref(cached), ctypes.byref(replays)), "sf_graph_stats")
+        return cached.value, replays.value
 
     def timing_enable(self, kc, on=True):
         _check(load_library().sf_timing_enable(self._h, int(kc), 1 if on else 0), "sf_timing_enable")

@@ -103,6 +103,16 @@ struct sf_model {
   void *ctxA = nullptr, *kx = nullptr, *vTx = nullptr;
   int ldv = 0, ldvx = 0;
   Timing timing[SF_KC_COUNT];
+  // graph replay: captured launch sequences keyed by the call's arguments
+  struct GraphEntry {
+    std::vector<char> key;
+    hipGraphExec_t exec = nullptr;
+    unsigned long long used = 0;
+  };
+  bool graph_on = false;
+  std::vector<GraphEntry> graphs;
+  unsigned long long graph_clock = 0;
+  long graph_replays = 0;
 };
 
 namespace {
@@ -479,6 +489,90 @@ int fail_alloc_after() {
   return e ? std::atoi(e) : -1;
 }
 
+// ---------------------------------------------------------------- graph replay
+constexpr size_t kMaxGraphs = 64;
+
+template <typename T>
+void key_put(std::vector<char>& k, const T& v) {
+  const char* p = reinterpret_cast<const char*>(&v);
+  k.insert(k.end(), p, p + sizeof(T));
+}
+
+std::vector<char> call_key(int kind, const void* a, const void* b, const void* c, const void* d, int B,
+                           const float* t, const float* dt, const sf_cond* cond, hipStream_t s) {
+  std::vector<char> k;
+  key_put(k, kind);
+  key_put(k, a);
+  key_put(k, b);
+  key_put(k, c);
+  key_put(k, d);
+  key_put(k, B);
+  key_put(k, (const void*)s);
+  for (int i = 0; i < B; ++i) key_put(k, t[i]);
+  if (dt)
+    for (int i = 0; i < B; ++i) key_put(k, dt[i]);
+  const bool has = cond != nullptr;
+  key_put(k, has);
+  if (has) {
+    key_put(k, (const void*)cond->ctx);
+    key_put(k, (const void*)cond->null_ctx);
+    key_put(k, cond->guidance);
+  }
+  return k;
+}
+
+bool any_timing(const sf_model* m) {
+  for (const Timing& tm : m->timing)
+    if (tm.on) return true;
+  return false;
+}
+
+void drop_graphs(sf_model* m) {
+  for (auto& g : m->graphs)
+    if (g.exec) (void)hipGraphExecDestroy(g.exec);
+  m->graphs.clear();
+}
+
+// Runs `enqueue` (which launches the call's kernels on s) through the graph cache: a
+// cached graph for `key` is replayed; otherwise the launches are captured, instantiated,
+// cached and replayed. Eager when graphs are off, on the null stream, or while timing.
+template <typename F>
+int run_graphed(sf_model* m, const std::vector<char>& key, hipStream_t s, F&& enqueue) {
+  if (!m->graph_on || s == nullptr || any_timing(m)) return enqueue();
+  for (auto& g : m->graphs) {
+    if (g.key == key) {
+      g.used = ++m->graph_clock;
+      ++m->graph_replays;
+      return hipGraphLaunch(g.exec, s) == hipSuccess ? SF_OK : SF_E_HIP;
+    }
+  }
+  if (hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal) != hipSuccess) return SF_E_HIP;
+  const int rc = enqueue();
+  hipGraph_t graph = nullptr;
+  const hipError_t ec = hipStreamEndCapture(s, &graph);
+  if (rc != SF_OK || ec != hipSuccess || !graph) {
+    if (graph) (void)hipGraphDestroy(graph);
+    return rc != SF_OK ? rc : SF_E_HIP;
+  }
+  hipGraphExec_t exec = nullptr;
+  const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  if (ei != hipSuccess || !exec) return SF_E_HIP;
+  if (m->graphs.size() >= kMaxGraphs) {
+    auto lru = m->graphs.begin();
+    for (auto it = m->graphs.begin(); it != m->graphs.end(); ++it)
+      if (it->used < lru->used) lru = it;
+    (void)hipGraphExecDestroy(lru->exec);
+    m->graphs.erase(lru);
+  }
+  sf_model::GraphEntry e;
+  e.key = key;
+  e.exec = exec;
+  e.used = ++m->graph_clock;
+  m->graphs.push_back(std::move(e));
+  return hipGraphLaunch(exec, s) == hipSuccess ? SF_OK : SF_E_HIP;
+}
+
 }  // namespace
 
 extern "C" {
@@ -571,6 +665,7 @@ int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows
 void sf_free(sf_model* m) {
   if (!m) return;
   if (m->wmem || m->wsmem) (void)hipDeviceSynchronize();
+  drop_graphs(m);
   for (auto& tm : m->timing)
     for (hipEvent_t e : tm.ev) (void)hipEventDestroy(e);
   if (m->wmem) (void)hipFree(m->wmem);
@@ -598,9 +693,11 @@ int sf_velocity(sf_model* m, const float* x, const float* t, int B, const sf_con
   const int rows = rows_for(m, B, cond, &guided, &w);
   if (!rows) return SF_E_INVAL;
   hipStream_t s = (hipStream_t)stream;
-  SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, guided ? m->vrows : v, s));
-  if (guided) return timed(m, SF_KC_EULER, s, [&]() { return sf::launch_cfg_combine(m->vrows, B, m->E, w, v, s); });
-  return SF_OK;
+  return run_graphed(m, call_key(0, x, v, nullptr, nullptr, B, t, nullptr, cond, s), s, [&]() -> int {
+    SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, guided ? m->vrows : v, s));
+    if (guided) return timed(m, SF_KC_EULER, s, [&]() { return sf::launch_cfg_combine(m->vrows, B, m->E, w, v, s); });
+    return SF_OK;
+  });
 }
 
 int sf_stream_step(sf_model* m, float* x, const float* t, const float* dt, int B, const sf_cond* cond,
@@ -613,13 +710,15 @@ int sf_stream_step(sf_model* m, float* x, const float* t, const float* dt, int B
   const int rows = rows_for(m, B, cond, &guided, &w);
   if (!rows) return SF_E_INVAL;
   hipStream_t s = (hipStream_t)stream;
-  SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, m->vrows, s));
-  return timed(m, SF_KC_EULER, s, [&]() {
-    sf::EulerArgs a{};
-    a.x = x; a.v = m->vrows; a.B = B; a.E = m->E; a.guided = guided ? 1 : 0; a.w = w;
-    for (int i = 0; i < B; ++i) a.dt.v[i] = dt[i];
-    a.z_new = z_new; a.x_done = x_done;
-    return sf::launch_euler_shift(a, s);
+  return run_graphed(m, call_key(1, x, z_new, x_done, nullptr, B, t, dt, cond, s), s, [&]() -> int {
+    SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, m->vrows, s));
+    return timed(m, SF_KC_EULER, s, [&]() {
+      sf::EulerArgs a{};
+      a.x = x; a.v = m->vrows; a.B = B; a.E = m->E; a.guided = guided ? 1 : 0; a.w = w;
+      for (int i = 0; i < B; ++i) a.dt.v[i] = dt[i];
+      a.z_new = z_new; a.x_done = x_done;
+      return sf::launch_euler_shift(a, s);
+    });
   });
 }
 
@@ -714,6 +813,24 @@ int sf_timing_read(sf_model* m, int kc, double* total_ms, long* launches) {
   *launches = tm.used;
   tm.used = 0;
   tm.launches = 0;
+  return SF_OK;
+}
+
+int sf_graph_enable(sf_model* m, int enable) {
+  if (!m) return SF_E_NOTLOADED;
+  if (!enable && !m->graphs.empty()) {
+    if (hipDeviceSynchronize() != hipSuccess) return SF_E_HIP;
+    drop_graphs(m);
+  }
+  m->graph_on = enable != 0;
+  return SF_OK;
+}
+
+int sf_graph_stats(const sf_model* m, int* cached, long* replays) {
+  if (!m) return SF_E_NOTLOADED;
+  if (!cached || !replays) return SF_E_INVAL;
+  *cached = (int)m->graphs.size();
+  *replays = m->graph_replays;
   return SF_OK;
 }
 

@@ -72,6 +72,7 @@ def test_calls_reject_null_handle_and_arguments():
     t = (ctypes.c_float * 4)(1, 0.75, 0.5, 0.25)
     dummy = ctypes.c_void_p(16)
     assert L.sf_velocity(None, dummy, t, 4, None, dummy, None) == -3
+    assert L.sf_graph_enable(None, 1) == -3
     assert L.sf_stream_step(None, dummy, t, t, 4, None, dummy, None, None) == -3
     assert L.sf_euler_shift(None, dummy, dummy, t, 4, dummy, None, None) == -3
     assert L.sf_modulation(None, t, 4, dummy, None) == -3
