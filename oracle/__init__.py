@@ -15,7 +15,10 @@ What it computes (StreamFlow, arXiv 2511.22009):
     (Sec. 3.1.1 discretization; Alg. 1, its final update);
   * the queue shift: new noise enters slot 0, every latent moves one slot on, and the
     oldest leaves once the pipeline is full (Sec. 3.4.1-3.4.2; Alg. 2);
-  * the whole Alg. 2 driver over M images.
+  * the whole Alg. 2 driver over M images;
+  * PeRFlow's time-window conversion of a noise prediction into a velocity, batched
+    over heterogeneous timesteps (Sec. 2 time windows; Sec. 3.3; Alg. 1), in
+    `oracle.perflow`.
 
 The network itself is not in the paper (the paper runs a pretrained UNet that
 predicts noise); this oracle uses a DiT-style adaLN transformer that outputs v
@@ -32,10 +35,11 @@ from .dit import (timestep_frequencies, timestep_embedding, modulation_table, pa
                   unpatchify, layer_norm, gelu_tanh, silu, attention, residual_one, forward_one,
                   velocity)
 from .stream import euler, stream_step, run_stream, sequential_sample
+from . import perflow
 
 __all__ = [
     "OracleModel", "load_blob", "timestep_frequencies", "timestep_embedding",
     "modulation_table", "patchify", "unpatchify", "layer_norm", "gelu_tanh", "silu",
     "attention", "residual_one", "forward_one", "velocity", "euler", "stream_step", "run_stream",
-    "sequential_sample",
+    "sequential_sample", "perflow",
 ]
