@@ -181,6 +181,40 @@ enum {
   SF_KC_COUNT
 };
 
+/* PeRFlow time windows (Sec. 2 time-window mechanism; Sec. 3.3 vectorized window lookup
+ * and batch parameters; Alg. 1). With a scheduler set, the network output of
+ * sf_stream_step is read as a noise prediction eps and each slot's update is
+ *   X_pred = lambda_t x + eta_t eps;  v = (X_pred - x) / (t^e - t);  x' = x + dt v
+ * with the window of t found as k = #{j < windows : t > j / windows + eps} (at least 1),
+ * running from t^s = k / windows down to t^e = (k - 1) / windows,
+ * gamma = sqrt(abar(t^s) / abar(t^e)), lambda_s = 1 / gamma,
+ * eta_s = -sqrt(1 - gamma^2) / gamma, denom = lambda_s (t - t^s) + (t^e - t),
+ * lambda_t = lambda_s (t^e - t^s) / denom, eta_t = eta_s (t^e - t) / denom.
+ * t is normalised time in [0, 1] (1 = noise) and dt is signed. abar is alphas_cumprod of
+ * the scaled-linear schedule (beta on a linear grid in sqrt(beta) from beta_start to
+ * beta_end over train_steps steps), read at index round(u (train_steps - 1)). The
+ * per-slot coefficients are computed in fp64 on the GPU; x' = A x + B eps in fp32.
+ * Guidance, when present, combines the two noise predictions as it combines velocities. */
+typedef struct {
+  int windows;        /* number of equal windows over [0, 1], 1..4096 */
+  int train_steps;    /* length of the schedule, 2..1048576 (1000 for the latent diffusion models) */
+  float beta_start;   /* 0 < beta_start < beta_end < 1 (0.00085, 0.012) */
+  float beta_end;
+  double eps;         /* window lookup tolerance, 0 <= eps < 1 / windows (1e-6) */
+} sf_perflow;
+
+/* Set (p != NULL) or clear (p == NULL: Euler on the velocity, the default) the
+ * scheduler of sf_stream_step and sf_scheduler_shift. Synchronous: builds the schedule
+ * on the host in fp64 and uploads it (one device allocation, kept until sf_free).
+ * Drops cached graphs. SF_E_INVAL on out-of-range fields. */
+int sf_set_scheduler(sf_model* m, const sf_perflow* p);
+
+/* The update and shift of sf_stream_step alone, with the model's scheduler, for a
+ * given network output `out` [B][C][H][W] (a velocity without a scheduler, a noise
+ * prediction with one). t and dt are host [B]. Test hook and building block. */
+int sf_scheduler_shift(sf_model* m, float* x, const float* out, const float* t, const float* dt, int B,
+                       const float* z_new, float* x_done, void* hip_stream);
+
 /* Graph replay of the step (Sec. 3.5 asks for static execution of heterogeneous steps;
  * here t is data, so one captured launch sequence serves every mix of timesteps).
  * While enabled, sf_velocity and sf_stream_step capture their launches on the caller's

@@ -46,6 +46,11 @@ class Buffer(enum.IntEnum):
     TABLE = 7
 
 
+class _PeRFlow(ctypes.Structure):
+    _fields_ = [("windows", ctypes.c_int), ("train_steps", ctypes.c_int), ("beta_start", ctypes.c_float),
+                ("beta_end", ctypes.c_float), ("eps", ctypes.c_double)]
+
+
 class SFError(RuntimeError):
     def __init__(self, code, where):
         self.code = code
@@ -81,6 +86,8 @@ _SIGS = {
     "sf_timing_enable": (_I, [_P, _I, _I]),
     "sf_timing_read": (_I, [_P, _I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_long)]),
     "sf_graph_enable": (_I, [_P, _I]),
+    "sf_set_scheduler": (_I, [_P, ctypes.POINTER(_PeRFlow)]),
+    "sf_scheduler_shift": (_I, [_P, _P, _P, _P, _P, _I, _P, _P, _P]),
     "sf_graph_stats": (_I, [_P, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_long)]),
 }
 
@@ -251,6 +258,24 @@ class Model:
                                             out.numel() * out.element_size(), self._stream(stream)),
                "sf_debug_read")
         return out.float()
+
+    def set_scheduler(self, windows=4, train_steps=1000, beta_start=0.00085, beta_end=0.012, eps=1e-6):
+        """Read the network output as a noise prediction and update with PeRFlow's time
+        windows (see sf_set_scheduler)."""
+        p = _PeRFlow(int(windows), int(train_steps), float(beta_start), float(beta_end), float(eps))
+        _check(load_library().sf_set_scheduler(self._h, ctypes.byref(p)), "sf_set_scheduler")
+
+    def clear_scheduler(self):
+        _check(load_library().sf_set_scheduler(self._h, None), "sf_set_scheduler")
+
+    def scheduler_shift(self, x, out, t, dt, B, z_new, x_done=None, stream=None):
+        """The update + shift of a stream step for a given network output `out`."""
+        tt, dd = _host_f32(t, B, "t"), _host_f32(dt, B, "dt")
+        need = B if x_done is not None else B + 1
+        done = self._latents(x_done, 1, "x_done") if x_done is not None else None
+        _check(load_library().sf_scheduler_shift(self._h, self._latents(x, need, "x"), self._latents(out, B, "out"),
+                                                 _ptr(tt), _ptr(dd), B, self._latents(z_new, 1, "z_new"), done,
+                                                 self._stream(stream)), "sf_scheduler_shift")
 
     def graph_enable(self, on=True):
         """Capture each distinct velocity / stream-step call into a HIP graph and replay it

@@ -2,6 +2,10 @@
 // final update of Alg. 1, with each slot's own signed step dt_k = t_next - t) fused
 // with the pipeline shift of Alg. 2 (fresh noise enters slot 0, every latent moves one
 // slot on, the oldest leaves finished), and the guidance combine v = v_u + w (v_c - v_u).
+// With time windows set, the network output is a noise prediction and the update is
+// PeRFlow's window conversion (Sec. 2 time windows, Sec. 3.3, Alg. 1): per slot,
+// x' = x + dt (lambda_t x + eta_t eps - x) / (t^e - t) = A_k x + B_k eps, with A_k and
+// B_k computed once per slot in fp64 at the start of every workgroup.
 //
 // In place without a race: each thread owns four elements of the latent and walks the
 // slots from the oldest to the newest, reading slot k before it writes slot k + 1.
@@ -17,8 +21,36 @@ __device__ __forceinline__ float4 guided(float4 vc, float4 vu, float w) {
                      vu.w + w * (vc.w - vu.w));
 }
 
+// Window coefficients of one slot at normalised time t with step dt: the window is
+// k = #{j < W : t > j / W + eps} (at least 1), running from t^s = k / W down to
+// t^e = (k - 1) / W; gamma = sqrt(abar(t^s) / abar(t^e)) with abar read at index
+// round(u (n - 1)); lambda_s = 1 / gamma, eta_s = -sqrt(1 - gamma^2) / gamma;
+// denom = lambda_s (t - t^s) + (t^e - t); lambda_t = lambda_s (t^e - t^s) / denom,
+// eta_t = eta_s (t^e - t) / denom; with c = dt / (t^e - t): A = 1 + c (lambda_t - 1),
+// B = c eta_t.
+__device__ void window_coeffs(const EulerArgs& a, int k, float* A, float* B) {
+  const double t = a.t.v[k], dt = a.dt.v[k];
+  int kw = 0;
+  for (int j = 0; j < a.windows; ++j) kw += t > (double)j / a.windows + a.eps ? 1 : 0;
+  kw = kw < 1 ? 1 : kw;
+  const double ts = (double)kw / a.windows, te = (double)(kw - 1) / a.windows;
+  const double as = a.abar[(int)rint(ts * (a.n_abar - 1))], ae = a.abar[(int)rint(te * (a.n_abar - 1))];
+  const double g = sqrt(as / ae);
+  const double lam_s = 1.0 / g, eta_s = -sqrt(1.0 - g * g) / g;
+  const double den = lam_s * (t - ts) + (te - t);
+  const double lam_t = lam_s * (te - ts) / den, eta_t = eta_s * (te - t) / den;
+  const double c = dt / (te - t);
+  *A = (float)(1.0 + c * (lam_t - 1.0));
+  *B = (float)(c * eta_t);
+}
+
 __global__ __launch_bounds__(256) void euler_shift_kernel(EulerArgs a) {
 #pragma clang fp contract(off)
+  __shared__ float coef[2][kMaxRows];
+  if (a.windows > 0) {
+    if (threadIdx.x < a.B) window_coeffs(a, threadIdx.x, &coef[0][threadIdx.x], &coef[1][threadIdx.x]);
+    __syncthreads();
+  }
   const int e4 = blockIdx.x * blockDim.x + threadIdx.x;
   const int n4 = a.E >> 2;
   if (e4 >= n4) return;
@@ -28,8 +60,14 @@ __global__ __launch_bounds__(256) void euler_shift_kernel(EulerArgs a) {
     float4 vk = v[(size_t)k * n4 + e4];
     if (a.guided) vk = guided(vk, v[(size_t)(a.B + k) * n4 + e4], a.w);
     const float4 xk = x[(size_t)k * n4 + e4];
-    const float d = a.dt.v[k];
-    const float4 xn = make_float4(xk.x + d * vk.x, xk.y + d * vk.y, xk.z + d * vk.z, xk.w + d * vk.w);
+    float4 xn;
+    if (a.windows > 0) {
+      const float A = coef[0][k], B = coef[1][k];
+      xn = make_float4(A * xk.x + B * vk.x, A * xk.y + B * vk.y, A * xk.z + B * vk.z, A * xk.w + B * vk.w);
+    } else {
+      const float d = a.dt.v[k];
+      xn = make_float4(xk.x + d * vk.x, xk.y + d * vk.y, xk.z + d * vk.z, xk.w + d * vk.w);
+    }
     if (k == a.B - 1 && a.x_done)
       ((float4*)a.x_done)[e4] = xn;
     else

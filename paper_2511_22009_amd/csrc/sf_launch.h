@@ -162,6 +162,14 @@ struct EulerArgs {
   RowScalars dt;
   const float* z_new;   // [E]
   float* x_done;        // [E] or nullptr (filling: the queue grows to B+1)
+  // windows > 0: v is a noise prediction and the update is the time-window conversion
+  // (x' = x + dt (lambda_t x + eta_t v - x) / (t^e - t)), per slot from t, the window
+  // count, the lookup tolerance and alphas_cumprod [n_abar] (fp64)
+  int windows;
+  double eps;
+  const double* abar;
+  int n_abar;
+  RowScalars t;
 };
 hipError_t launch_euler_shift(const EulerArgs& a, hipStream_t s);
 // v_out[k] = v[B+k] + w (v[k] - v[B+k]) for k < B.

@@ -109,6 +109,11 @@ struct sf_model {
     hipGraphExec_t exec = nullptr;
     unsigned long long used = 0;
   };
+  // PeRFlow time windows (windows == 0: Euler on the velocity)
+  int windows = 0;
+  double win_eps = 0.0;
+  double* abar = nullptr;
+  int n_abar = 0;
   bool graph_on = false;
   std::vector<GraphEntry> graphs;
   unsigned long long graph_clock = 0;
@@ -489,6 +494,16 @@ int fail_alloc_after() {
   return e ? std::atoi(e) : -1;
 }
 
+// Copies the model's time-window scheduler (if any) and the slots' times into the
+// update's arguments.
+void set_windows(const sf_model* m, const float* t, int B, sf::EulerArgs& a) {
+  a.windows = m->windows;
+  a.eps = m->win_eps;
+  a.abar = m->abar;
+  a.n_abar = m->n_abar;
+  for (int i = 0; i < B; ++i) a.t.v[i] = t[i];
+}
+
 // ---------------------------------------------------------------- graph replay
 constexpr size_t kMaxGraphs = 64;
 
@@ -666,6 +681,7 @@ void sf_free(sf_model* m) {
   if (!m) return;
   if (m->wmem || m->wsmem) (void)hipDeviceSynchronize();
   drop_graphs(m);
+  if (m->abar) (void)hipFree(m->abar);
   for (auto& tm : m->timing)
     for (hipEvent_t e : tm.ev) (void)hipEventDestroy(e);
   if (m->wmem) (void)hipFree(m->wmem);
@@ -717,6 +733,7 @@ int sf_stream_step(sf_model* m, float* x, const float* t, const float* dt, int B
       a.x = x; a.v = m->vrows; a.B = B; a.E = m->E; a.guided = guided ? 1 : 0; a.w = w;
       for (int i = 0; i < B; ++i) a.dt.v[i] = dt[i];
       a.z_new = z_new; a.x_done = x_done;
+      set_windows(m, t, B, a);
       return sf::launch_euler_shift(a, s);
     });
   });
@@ -832,6 +849,64 @@ int sf_graph_stats(const sf_model* m, int* cached, long* replays) {
   *cached = (int)m->graphs.size();
   *replays = m->graph_replays;
   return SF_OK;
+}
+
+int sf_set_scheduler(sf_model* m, const sf_perflow* p) {
+  if (!m) return SF_E_NOTLOADED;
+  if (!p) {
+    if (m->windows != 0 && !m->graphs.empty()) {
+      if (hipDeviceSynchronize() != hipSuccess) return SF_E_HIP;
+      drop_graphs(m);
+    }
+    m->windows = 0;
+    return SF_OK;
+  }
+  if (p->windows < 1 || p->windows > 4096 || p->train_steps < 2 || p->train_steps > (1 << 20) ||
+      !(p->beta_start > 0.0f) || !(p->beta_end > p->beta_start) || !(p->beta_end < 1.0f) ||
+      !(p->eps >= 0.0) || !(p->eps < 1.0 / p->windows))
+    return SF_E_INVAL;
+  // scaled-linear schedule: sqrt(beta) on a linear grid (start + i * step, the last
+  // point exactly the end), beta = its square, alphas_cumprod = running product of 1 - beta
+  const int T = p->train_steps;
+  const double s0 = std::sqrt((double)p->beta_start), s1 = std::sqrt((double)p->beta_end);
+  const double step = (s1 - s0) / (double)(T - 1);
+  std::vector<double> ab((size_t)T);
+  double prod = 1.0;
+  for (int i = 0; i < T; ++i) {
+    const double sb = i == T - 1 ? s1 : (double)i * step + s0;
+    prod *= 1.0 - sb * sb;
+    ab[(size_t)i] = prod;
+  }
+  if (hipDeviceSynchronize() != hipSuccess) return SF_E_HIP;
+  drop_graphs(m);
+  if (m->n_abar != T) {
+    if (m->abar) (void)hipFree(m->abar);
+    m->abar = nullptr;
+    m->n_abar = 0;
+    if (hipMalloc((void**)&m->abar, sizeof(double) * (size_t)T) != hipSuccess) return SF_E_OOM;
+    m->n_abar = T;
+  }
+  if (hipMemcpy(m->abar, ab.data(), sizeof(double) * (size_t)T, hipMemcpyHostToDevice) != hipSuccess)
+    return SF_E_HIP;
+  m->windows = p->windows;
+  m->win_eps = p->eps;
+  return SF_OK;
+}
+
+int sf_scheduler_shift(sf_model* m, float* x, const float* out, const float* t, const float* dt, int B,
+                       const float* z_new, float* x_done, void* stream) {
+  if (!m) return SF_E_NOTLOADED;
+  if (!x || !out || !t || !dt || !z_new || B < 1 || B > SF_MAX_ROWS || !finite_all(t, B) || !finite_all(dt, B))
+    return SF_E_INVAL;
+  hipStream_t s = (hipStream_t)stream;
+  return timed(m, SF_KC_EULER, s, [&]() {
+    sf::EulerArgs a{};
+    a.x = x; a.v = out; a.B = B; a.E = m->E; a.guided = 0; a.w = 0.0f;
+    for (int i = 0; i < B; ++i) a.dt.v[i] = dt[i];
+    a.z_new = z_new; a.x_done = x_done;
+    set_windows(m, t, B, a);
+    return sf::launch_euler_shift(a, s);
+  });
 }
 
 }  // extern "C"
