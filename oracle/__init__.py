@@ -34,12 +34,12 @@ from .weights import OracleModel, load_blob
 from .dit import (timestep_frequencies, timestep_embedding, modulation_table, patchify,
                   unpatchify, layer_norm, gelu_tanh, silu, attention, residual_one, forward_one,
                   velocity)
-from .stream import euler, stream_step, run_stream, sequential_sample
+from .stream import euler, stream_step, run_stream, sequential_sample, noise_latent
 from . import perflow
 
 __all__ = [
     "OracleModel", "load_blob", "timestep_frequencies", "timestep_embedding",
     "modulation_table", "patchify", "unpatchify", "layer_norm", "gelu_tanh", "silu",
     "attention", "residual_one", "forward_one", "velocity", "euler", "stream_step", "run_stream",
-    "sequential_sample", "perflow",
+    "sequential_sample", "noise_latent", "perflow",
 ]

@@ -63,6 +63,17 @@ def run_stream(m, grid, M, noise, ctx_of=None, null_ctx=None, guidance=None, dty
     return images[:M]
 
 
+def noise_latent(x_ref, z, t0):
+    """The point of the straight path between a reference latent and noise at time t0
+    (Sec. 2: x_t on the line from data to noise; here t = 1 is noise):
+    x = (1 - t0) x_ref + t0 z, each product and the sum rounded to fp32. With a schedule
+    that starts at t0 < 1, this is the latent an image-to-image run admits (the paper's
+    img2img workload); t0 = 1 gives z itself."""
+    t0 = np.float32(t0)
+    a = np.float32(1.0) - t0
+    return (a * np.asarray(x_ref, dtype=np.float32) + t0 * np.asarray(z, dtype=np.float32)).astype(np.float32)
+
+
 def sequential_sample(m, z, grid, ctx=None, null_ctx=None, guidance=None, dtype=np.float32):
     """One image alone: x <- x + dt_i F(x, t_i) over the grid, from noise z."""
     grid = np.asarray(grid, dtype=np.float32)

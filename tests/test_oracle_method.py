@@ -157,3 +157,43 @@ def test_fill_phase_grows_queue():
     assert done is None and xn.shape[0] == 3
     np.testing.assert_array_equal(xn[0], z)
     np.testing.assert_array_equal(xn[1:], oracle.euler(x, v, dt[:2]))
+
+
+# ------------------------------------------------- image-to-image and one-step runs
+
+def test_noise_latent_endpoints_and_line():
+    """x = (1 - t0) x_ref + t0 z: t0 = 1 gives z, t0 = 0 gives x_ref, and at dyadic t0 on
+    dyadic data the point is exact."""
+    rng = np.random.default_rng(21)
+    ref = (rng.integers(-64, 65, (4, 8, 8)) / 16.0).astype(np.float32)
+    z = (rng.integers(-64, 65, (4, 8, 8)) / 16.0).astype(np.float32)
+    np.testing.assert_array_equal(oracle.noise_latent(ref, z, 1.0), z)
+    np.testing.assert_array_equal(oracle.noise_latent(ref, z, 0.0), ref)
+    np.testing.assert_array_equal(oracle.noise_latent(ref, z, 0.25), 0.75 * ref + 0.25 * z)
+    mid = oracle.noise_latent(ref, z, 0.5)
+    np.testing.assert_array_equal(mid - ref, 0.5 * (z - ref))
+
+
+def test_img2img_stream_equals_sequential_from_the_noised_reference():
+    """A schedule starting at t0 < 1 with noised references admitted: every image equals
+    the one-image sampler started from its own noised reference."""
+    cfg = W.get_config("tiny_tsens")
+    m = oracle.load_blob(W.make_blob(cfg))
+    grid = np.array([0.5, 0.25, 0.0], np.float32)
+    refs = {j: W.latents(cfg, 1, seed=500 + j)[0] for j in range(1, 8)}
+    noisy = lambda j: oracle.noise_latent(refs[j], W.z_new_for_image(cfg, j), grid[0])  # noqa: E731
+    imgs = oracle.run_stream(m, grid, 4, noisy)
+    for i, img in enumerate(imgs):
+        np.testing.assert_array_equal(img, oracle.sequential_sample(m, noisy(i + 1), grid))
+
+
+def test_one_step_queue():
+    """K = 1: every call finishes one image in a single Euler step from t = 1 to 0."""
+    cfg = W.get_config("tiny_tsens")
+    m = oracle.load_blob(W.make_blob(cfg))
+    grid = np.array([1.0, 0.0], np.float32)
+    imgs = oracle.run_stream(m, grid, 3, lambda j: W.z_new_for_image(cfg, j))
+    for i, img in enumerate(imgs):
+        z = W.z_new_for_image(cfg, i + 1)
+        v = oracle.velocity(m, z[None], grid[:1])[0]
+        np.testing.assert_array_equal(img, z + np.float32(-1.0) * v)
