@@ -181,6 +181,13 @@ enum {
   SF_KC_COUNT
 };
 
+/* The latent an image-to-image run admits: the point of the straight path between a
+ * reference latent and noise at the schedule's first time t0 (Sec. 2 straight paths;
+ * t = 1 is noise): out = (1 - t0) x_ref + t0 z, products and sum rounded to fp32
+ * separately. x_ref, z, out: device [C][H][W]; out may alias z or x_ref (element-wise).
+ * t0 in [0, 1]. Pass `out` as z_new of sf_stream_step with a schedule starting at t0. */
+int sf_noise_latent(sf_model* m, const float* x_ref, const float* z, float t0, float* out, void* hip_stream);
+
 /* PeRFlow time windows (Sec. 2 time-window mechanism; Sec. 3.3 vectorized window lookup
  * and batch parameters; Alg. 1). With a scheduler set, the network output of
  * sf_stream_step is read as a noise prediction eps and each slot's update is

@@ -86,6 +86,7 @@ _SIGS = {
     "sf_timing_enable": (_I, [_P, _I, _I]),
     "sf_timing_read": (_I, [_P, _I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_long)]),
     "sf_graph_enable": (_I, [_P, _I]),
+    "sf_noise_latent": (_I, [_P, _P, _P, ctypes.c_float, _P, _P]),
     "sf_set_scheduler": (_I, [_P, ctypes.POINTER(_PeRFlow)]),
     "sf_scheduler_shift": (_I, [_P, _P, _P, _P, _P, _I, _P, _P, _P]),
     "sf_graph_stats": (_I, [_P, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_long)]),
@@ -276,6 +277,16 @@ class Model:
         _check(load_library().sf_scheduler_shift(self._h, self._latents(x, need, "x"), self._latents(out, B, "out"),
                                                  _ptr(tt), _ptr(dd), B, self._latents(z_new, 1, "z_new"), done,
                                                  self._stream(stream)), "sf_scheduler_shift")
+
+    def noise_latent(self, x_ref, z, t0, out=None, stream=None):
+        """out = (1 - t0) x_ref + t0 z: the admitted latent of an image-to-image run."""
+        import torch
+        if out is None:
+            out = torch.empty_like(z)
+        _check(load_library().sf_noise_latent(self._h, self._latents(x_ref, 1, "x_ref"), self._latents(z, 1, "z"),
+                                              float(t0), self._latents(out, 1, "out"), self._stream(stream)),
+               "sf_noise_latent")
+        return out
 
     def graph_enable(self, on=True):
         """Capture each distinct velocity / stream-step call into a HIP graph and replay it

@@ -98,4 +98,22 @@ hipError_t launch_cfg_combine(const float* v, int B, int E, float w, float* v_ou
   return hipGetLastError();
 }
 
+// The admitted latent of an image-to-image run: the straight-path point between the
+// reference and the noise at the schedule's first time t0 (t = 1 is noise).
+__global__ __launch_bounds__(256) void noise_latent_kernel(const float* x_ref, const float* z, float t0, int n4,
+                                                            float* out) {
+#pragma clang fp contract(off)
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  const float a = 1.0f - t0;
+  const float4 r = ((const float4*)x_ref)[i], q = ((const float4*)z)[i];
+  ((float4*)out)[i] = make_float4(a * r.x + t0 * q.x, a * r.y + t0 * q.y, a * r.z + t0 * q.z, a * r.w + t0 * q.w);
+}
+
+hipError_t launch_noise_latent(const float* x_ref, const float* z, float t0, int E, float* out, hipStream_t s) {
+  const int n4 = E >> 2;
+  launch(noise_latent_kernel, dim3((n4 + 255) / 256), dim3(256), 0, s, x_ref, z, t0, n4, out);
+  return hipGetLastError();
+}
+
 }  // namespace sf

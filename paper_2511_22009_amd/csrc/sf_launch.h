@@ -174,5 +174,7 @@ struct EulerArgs {
 hipError_t launch_euler_shift(const EulerArgs& a, hipStream_t s);
 // v_out[k] = v[B+k] + w (v[k] - v[B+k]) for k < B.
 hipError_t launch_cfg_combine(const float* v, int B, int E, float w, float* v_out, hipStream_t s);
+// out = (1 - t0) x_ref + t0 z, each product and the sum rounded separately
+hipError_t launch_noise_latent(const float* x_ref, const float* z, float t0, int E, float* out, hipStream_t s);
 
 }  // namespace sf

@@ -909,4 +909,10 @@ int sf_scheduler_shift(sf_model* m, float* x, const float* out, const float* t, 
   });
 }
 
+int sf_noise_latent(sf_model* m, const float* x_ref, const float* z, float t0, float* out, void* stream) {
+  if (!m) return SF_E_NOTLOADED;
+  if (!x_ref || !z || !out || !(t0 >= 0.0f && t0 <= 1.0f)) return SF_E_INVAL;
+  return sf::launch_noise_latent(x_ref, z, t0, m->E, out, (hipStream_t)stream) == hipSuccess ? SF_OK : SF_E_HIP;
+}
+
 }  // extern "C"

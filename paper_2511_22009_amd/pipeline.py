@@ -58,11 +58,16 @@ class StreamQueue:
         return done_out
 
 
-def run_images(model, grid, M, noise, contexts_of=None, null_ctx=None, guidance=None):
+def run_images(model, grid, M, noise, contexts_of=None, null_ctx=None, guidance=None, references=None):
     """Generate M latents with Alg. 2: M + K - 1 stream steps. noise(j) gives image j's
-    noise as a device tensor; contexts_of(j) its context when conditioned."""
+    noise as a device tensor; contexts_of(j) its context when conditioned. With
+    references(j) (image-to-image), image j enters as the straight-path point between its
+    reference and its noise at grid[0] (sf_noise_latent); the grid then starts at t0 < 1."""
     import torch
     K = len(grid) - 1
+    if references is not None:
+        raw, t0 = noise, float(grid[0])
+        noise = lambda j: model.noise_latent(references(j), raw(j), t0)  # noqa: E731
     ctx_buf = None
     if contexts_of is not None:
         c1 = contexts_of(1)

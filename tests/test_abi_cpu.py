@@ -74,6 +74,7 @@ def test_calls_reject_null_handle_and_arguments():
     assert L.sf_velocity(None, dummy, t, 4, None, dummy, None) == -3
     assert L.sf_graph_enable(None, 1) == -3
     assert L.sf_set_scheduler(None, None) == -3
+    assert L.sf_noise_latent(None, dummy, dummy, 0.5, dummy, None) == -3
     assert L.sf_stream_step(None, dummy, t, t, 4, None, dummy, None, None) == -3
     assert L.sf_euler_shift(None, dummy, dummy, t, 4, dummy, None, None) == -3
     assert L.sf_modulation(None, t, 4, dummy, None) == -3

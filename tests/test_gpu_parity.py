@@ -276,3 +276,43 @@ def test_guidance_weight_zero_gives_unconditional_rows():
     v0 = host(m.velocity(dev(x), t, Cond(dev(ctx), dev(nctx), 0.0)))
     vu = host(m.velocity(dev(x), t, Cond(dev(np.repeat(nctx[None], cfg.K, 0)), None, 0.0)))
     np.testing.assert_array_equal(v0, vu)
+
+
+# ------------------------------------------------- image-to-image and one-step runs
+
+def test_noise_latent_bit_exact():
+    cfg = W.get_config("tiny")
+    rng = np.random.default_rng(17)
+    ref = rng.standard_normal(cfg.latent_shape).astype(np.float32)
+    z = rng.standard_normal(cfg.latent_shape).astype(np.float32)
+    m = model("tiny", "fp32")
+    for t0 in (1.0, 0.0, 0.5, 0.37):
+        got = host(m.noise_latent(dev(ref), dev(z), t0))
+        np.testing.assert_array_equal(got, oracle.noise_latent(ref, z, t0))
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_img2img_stream_matches_oracle(prec):
+    """A schedule starting at t0 = 0.5 with noised references admitted through the
+    queue, against the oracle's Alg. 2 on the same noised inputs."""
+    from paper_2511_22009_amd.pipeline import run_images
+    cfg = W.get_config("tiny_tsens")
+    grid = np.array([0.5, 0.25, 0.0], np.float32)
+    refs = {j: W.latents(cfg, 1, seed=500 + j)[0] for j in range(1, 8)}
+    m = model("tiny_tsens", prec)
+    imgs = run_images(m, grid, 4, lambda j: dev(W.z_new_for_image(cfg, j)), references=lambda j: dev(refs[j]))
+    noisy = lambda j: oracle.noise_latent(refs[j], W.z_new_for_image(cfg, j), grid[0])  # noqa: E731
+    ref = oracle.run_stream(oracle_model("tiny_tsens"), grid, 4, noisy)
+    for i in range(4):
+        assert rel_l2(host(imgs[i]), ref[i]) <= 4 * TOL[prec]
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_one_step_queue_matches_oracle(prec):
+    from paper_2511_22009_amd.pipeline import run_images
+    cfg = W.get_config("tiny_tsens")
+    grid = np.array([1.0, 0.0], np.float32)
+    imgs = run_images(model("tiny_tsens", prec), grid, 3, lambda j: dev(W.z_new_for_image(cfg, j)))
+    ref = oracle.run_stream(oracle_model("tiny_tsens"), grid, 3, lambda j: W.z_new_for_image(cfg, j))
+    for i in range(3):
+        assert rel_l2(host(imgs[i]), ref[i]) <= TOL[prec]
