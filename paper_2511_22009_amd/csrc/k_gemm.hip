@@ -7,12 +7,14 @@
 //   GELU     out = GELU_tanh(acc + bias);
 //   RES      h += acc + bias.
 //
-// bf16 path: v_mfma_f32_32x32x16_bf16 on 128x128x64 workgroup tiles, four wavefronts
-// each owning a 64x64 sub-tile (2x2 MFMA blocks), both operand tiles double-buffered in
-// LDS with a 16-byte row pad so the 16-byte fragment reads of a 32-lane column are free
-// of bank conflicts, and the next K-slice fetched into registers while the current one
-// feeds the matrix cores. fp32 path: LDS-tiled FMA GEMM (exact fp32 arithmetic for
-// the parity mode).
+// bf16 path: v_mfma_f32_32x32x16_bf16 on BM x BN x 64 workgroup tiles (table at the
+// end), each wavefront owning a 64x64 or 64x96 sub-tile; both operand tiles are
+// double-buffered in LDS with a 16-byte row pad so the 16-byte fragment reads of a
+// 32-lane column are free of bank conflicts, and the next K-slice is fetched into
+// registers while the current one feeds the matrix cores. The MFMAs take the weight
+// fragment as the first operand, so each lane ends up holding four adjacent output
+// columns of one row, which the epilogues move in 8- and 16-byte pieces. fp32 path:
+// LDS-tiled FMA GEMM (exact fp32 arithmetic for the parity mode).
 #include <cmath>
 
 #include "sf_device.h"
@@ -188,6 +190,116 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const float* 
   }
 }
 
+// Epilogue of the bf16-output projections (GELU for the MLP up-projection, the head
+// split for QKV). Bias and activation are applied in registers, where every lane holds
+// four adjacent columns of one row; the bf16 results are staged in LDS (8-byte writes)
+// and leave in 16-byte chunks: 8 adjacent columns of a row for the GELU output and for
+// q / k (a chunk never straddles a head since the head width is a multiple of 8), and 8
+// adjacent tokens of one column for the transposed v.
+constexpr int kEpiPad = 8;  // bf16 row pad of the staged tile (16 bytes)
+
+template <EpiKind KIND, int BM, int BN, int TM, int TN, int NT>
+__device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&acc)[TM][TN], bf16* Cs,
+                                              const float* bias_s, int m0, int n0, int wm, int wn, int l32, int g,
+                                              int tid) {
+  constexpr int CPB = BN + kEpiPad;
+  f32x4 bias[TN][4];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) bias[j][q] = *(const f32x4*)&bias_s[(wn * TN + j) * 32 + q * 8 + g * 4];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int row = (wm * TM + i) * 32 + l32;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] = acc[i][j][4 * q + e] + bias[j][q][e];
+          if constexpr (KIND == EPI_GELU) v[e] = gelu_tanh(v[e]);
+        }
+        const bf16x4 o = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+        *(bf16x4*)&Cs[row * CPB + (wn * TN + j) * 32 + q * 8 + g * 4] = o;
+      }
+  }
+  __syncthreads();
+  // row-major 16-byte chunks: the whole GELU tile; the q and k columns of QKV
+  constexpr int C8 = BN / 8;
+  constexpr int TOTAL = BM * C8;
+  constexpr int IT = (TOTAL + NT - 1) / NT;
+  constexpr int U = batch_of(IT, 8);
+  for (int i0 = 0; i0 < IT; i0 += U) {
+    u32x4 val[U];
+    int mm[U], nn[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = tid + (i0 + u) * NT;
+      const int row = c / C8, c8 = c - row * C8;
+      const bool in = TOTAL % NT == 0 || c < TOTAL;
+      mm[u] = in ? m0 + row : a.M;
+      nn[u] = n0 + c8 * 8;
+      val[u] = *(const u32x4*)&Cs[(in ? row : 0) * CPB + c8 * 8];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int m = mm[u], n = nn[u];
+      if (m >= a.M || n >= a.N) continue;
+      if constexpr (KIND == EPI_GELU) {
+        *(u32x4*)((bf16*)a.out + (size_t)m * a.ldo + n) = val[u];
+      } else {
+        const int part = (int)fdiv((uint32_t)n, a.div_D);
+        const int which = a.which_base + part;
+        const int rem = n - part * a.D;
+        const int head = (int)fdiv((uint32_t)rem, a.div_dh);
+        const int d = rem - head * a.dh;
+        const int r = (int)fdiv((uint32_t)m, a.div_ntok);
+        const int tok = m - r * a.ntok;
+        bf16* base = (bf16*)(which == 0 ? a.q : a.k);
+        if (which < 2) *(u32x4*)(base + (((size_t)r * a.heads + head) * a.ntok + tok) * a.dh + d) = val[u];
+      }
+    }
+  }
+  if constexpr (KIND == EPI_QKV) {
+    // transposed v: item = (column, 8 consecutive rows); skipped unless the tile
+    // reaches the v columns
+    if (a.which_base + (int)fdiv((uint32_t)min(n0 + BN, a.N) - 1, a.div_D) < 2) return;
+    constexpr int R8 = BM / 8;
+    constexpr int VT = R8 * BN;
+    constexpr int VIT = (VT + NT - 1) / NT;
+    for (int it = 0; it < VIT; ++it) {
+      const int c = tid + it * NT;
+      const int r8 = c / BN, col = c - r8 * BN;  // adjacent lanes: adjacent columns
+      const int n = n0 + col, m = m0 + r8 * 8;
+      if ((VT % NT != 0 && c >= VT) || n >= a.N || m >= a.M) continue;
+      const int part = (int)fdiv((uint32_t)n, a.div_D);
+      if (a.which_base + part < 2) continue;
+      const int rem = n - part * a.D;
+      const int head = (int)fdiv((uint32_t)rem, a.div_dh);
+      const int d = rem - head * a.dh;
+      const int r = (int)fdiv((uint32_t)m, a.div_ntok);
+      const int tok = m - r * a.ntok;
+      const bf16* cp = Cs + (r8 * 8) * CPB + col;
+      bf16* vt = (bf16*)a.vT + (((size_t)r * a.heads + head) * a.dh + d) * a.ldv;
+      if (tok + 8 <= a.ntok && m + 8 <= a.M && (tok & 7) == 0) {
+        bf16x8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = cp[e * CPB];
+        *(bf16x8*)(vt + tok) = o;
+      } else {
+        for (int e = 0; e < 8 && m + e < a.M; ++e) {
+          const int me = m + e;
+          const int re = (int)fdiv((uint32_t)me, a.div_ntok);
+          const int te = me - re * a.ntok;
+          ((bf16*)a.vT)[(((size_t)re * a.heads + head) * a.dh + d) * a.ldv + te] = cp[e * CPB];
+        }
+      }
+    }
+  }
+}
+
 // Block -> tile map. The hardware hands workgroup b to XCD b % 8 and each XCD has its
 // own L2, so each XCD gets a contiguous range of logical tiles; inside it tiles go in
 // groups of kGroupM tile rows, M fastest, so the A rows and B columns a group touches
@@ -236,6 +348,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
   constexpr int C_BYTES = RP * CP * 4;
   constexpr int SMEM = AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES;
   static_assert(SMEM <= LDS_CAP, "tile does not fit in LDS");
+  static_assert(BM * (BN + kEpiPad) * 2 <= SMEM, "staged bf16 tile does not fit in LDS");
   constexpr int KS = kBK / 16;                 // MFMA K steps per tile
   constexpr int NMFMA = TM * TN * KS;
   constexpr int NDSR = (TM + TN) * KS;
@@ -253,6 +366,15 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
   int mt, nt;
   tile_coords((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
+  // the tile's bias columns go to LDS now, so the epilogue does not wait on them
+  constexpr bool kBf16Out = KIND == EPI_GELU || KIND == EPI_QKV;
+  __shared__ __attribute__((aligned(16))) float bias_s[kBf16Out ? BN : 4];
+  if constexpr (kBf16Out) {
+    for (int c = tid; c < BN / 4; c += NT) {
+      const int n = n0 + 4 * c;
+      *(f32x4*)&bias_s[4 * c] = n < a.N ? *(const f32x4*)(a.bias + n) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
 
   const __amdgpu_buffer_rsrc_t ra_src = buffer_rsrc(a.A, (uint32_t)a.M * a.lda * 2);
   const __amdgpu_buffer_rsrc_t rb_src = buffer_rsrc(a.B, (uint32_t)a.N * a.ldb * 2);
@@ -328,7 +450,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cb][i], bfr[cb][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cb][j], af[cb][i], acc[i][j], 0, 0, 0);
     }
     if (write_next) lstore(cur ^ 1);
     if (load_next) gload(kt + 2);
@@ -366,24 +488,31 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
   step(kt & 1, kt, false, false);
   __syncthreads();
 
-  float* Cs = (float*)smem;
+  // The MFMAs compute C^T blocks (weights as the first operand), so in acc[i][j]
+  // lane (l32, g) holds row (wm*TM + i)*32 + l32 of the tile and, in registers
+  // 4q..4q+3, the four adjacent columns (wn*TN + j)*32 + 8q + 4g + 0..3.
+  if constexpr (kBf16Out) {
+    bf16_epilogue<KIND, BM, BN, TM, TN, NT>(a, acc, (bf16*)smem, bias_s, m0, n0, wm, wn, l32, g, tid);
+  } else {
+    float* Cs = (float*)smem;
 #pragma unroll
-  for (int p = 0; p < NP; ++p) {
+    for (int p = 0; p < NP; ++p) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int rb0 = (wm * TM + i) * 32;
-      if (rb0 < p * RP || rb0 >= (p + 1) * RP) continue;
+      for (int i = 0; i < TM; ++i) {
+        const int rb0 = (wm * TM + i) * 32;
+        if (rb0 < p * RP || rb0 >= (p + 1) * RP) continue;
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = rb0 - p * RP + (r >> 2) * 8 + g * 4 + (r & 3);
-          Cs[row * CP + (wn * TN + j) * 32 + l32] = acc[i][j][r];
-        }
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            *(f32x4*)&Cs[(rb0 - p * RP + l32) * CP + (wn * TN + j) * 32 + q * 8 + g * 4] = v;
+          }
+      }
+      __syncthreads();
+      staged_epilogue<KIND, RP, BN, NT>(a, Cs, CP, m0 + p * RP, n0, tid);
+      if (p + 1 < NP) __syncthreads();
     }
-    __syncthreads();
-    staged_epilogue<KIND, RP, BN, NT>(a, Cs, CP, m0 + p * RP, n0, tid);
-    if (p + 1 < NP) __syncthreads();
   }
 }
 

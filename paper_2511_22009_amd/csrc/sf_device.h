@@ -78,12 +78,16 @@ template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf
 
 template <typename T> __device__ __forceinline__ float to_f32(T v) { return (float)v; }
 
-// tanh-form GELU written as z * sigmoid(2u), u = sqrt(2/pi) (z + 0.044715 z^3),
-// since 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)).
+// tanh-form GELU written as z * sigmoid(2u), u = sqrt(2/pi) (z + 0.044715 z^3), since
+// 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)); with exp(-2u) = 2^y, y = z (c0 + c1 z^2)
+// (log2(e) folded into the constants) it is five plain operations plus the hardware
+// exp2 and reciprocal (each within about 1 ulp). Both limits are exact: 2^y overflows to
+// inf for very negative z (result -0) and underflows to 0 for large z (result z).
 __device__ __forceinline__ float gelu_tanh(float z) {
-  const float k2 = 2.0f * 0.7978845608028654f;  // 2 sqrt(2/pi)
-  float u2 = k2 * (z + 0.044715f * z * z * z);
-  return z / (1.0f + __expf(-u2));
+  constexpr float c0 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
+  constexpr float c1 = c0 * 0.044715f;
+  const float y = z * __builtin_fmaf(c1, z * z, c0);
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(y));
 }
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
