@@ -56,8 +56,6 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int m, int n, float 
 }
 
 // ------------------------------------------------------------------ bf16 / MFMA
-constexpr int kBK = 64;
-constexpr int kLdk = kBK + 8;  // LDS row pitch in bf16 (144 bytes)
 
 __device__ __forceinline__ void store4(bf16* p, float a, float b, float c, float d) {
   const bf16x4 v = {(bf16)a, (bf16)b, (bf16)c, (bf16)d};
@@ -201,7 +199,7 @@ constexpr int kEpiPad = 8;  // bf16 row pad of the staged tile (16 bytes)
 template <EpiKind KIND, int BM, int BN, int TM, int TN, int NT>
 __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&acc)[TM][TN], bf16* Cs,
                                               const float* bias_s, int m0, int n0, int wm, int wn, int l32, int g,
-                                              int tid) {
+                                              bool owner, int tid) {
   constexpr int CPB = BN + kEpiPad;
   f32x4 bias[TN][4];
 #pragma unroll
@@ -210,6 +208,7 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
     for (int q = 0; q < 4; ++q) bias[j][q] = *(const f32x4*)&bias_s[(wn * TN + j) * 32 + q * 8 + g * 4];
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
+    if (!owner) break;
     const int row = (wm * TM + i) * 32 + l32;
 #pragma unroll
     for (int j = 0; j < TN; ++j)
@@ -330,17 +329,18 @@ __device__ __forceinline__ void tile_coords(int nbm, int nbn, int& mt, int& nt) 
 // instead of in stalls between them. Loader chunks past the tile (when the chunk count
 // is not a multiple of the thread count) read zeros and land in a spare LDS slot, so
 // the block stays branch-free.
-template <int BM, int BN, int WM, int WN, EpiKind KIND>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs a) {
-  constexpr int NT = WM * WN * 64;
+template <int BM, int BN, int BK, int WM, int WN, int KSPLIT, EpiKind KIND>
+__global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(GemmArgs a) {
+  constexpr int NT = WM * WN * KSPLIT * 64;
+  constexpr int LDK = BK + 8;  // LDS row pitch in bf16 (a 16-byte pad)
   constexpr int TM = BM / WM / 32;
   constexpr int TN = BN / WN / 32;
   static_assert(TM * WM * 32 == BM && TN * WN * 32 == BN, "wave grid must tile the block");
-  constexpr int CPR = kBK / 8;
+  constexpr int CPR = BK / 8;
   constexpr int ATOT = BM * CPR, BTOT = BN * CPR;
   constexpr int ACH = (ATOT + NT - 1) / NT;
   constexpr int BCH = (BTOT + NT - 1) / NT;
-  constexpr int AB_BYTES = 2 * (BM + BN) * kLdk * 2 + 16;  // + spare slot
+  constexpr int AB_BYTES = 2 * (BM + BN) * LDK * 2 + 16;  // + spare slot
   constexpr int CP = BN + 4;
   constexpr int LDS_CAP = 160 * 1024;
   constexpr int NP = (BM * CP * 4 <= LDS_CAP) ? 1 : ((BM / 2) * CP * 4 <= LDS_CAP ? 2 : 4);
@@ -349,19 +349,24 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
   constexpr int SMEM = AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES;
   static_assert(SMEM <= LDS_CAP, "tile does not fit in LDS");
   static_assert(BM * (BN + kEpiPad) * 2 <= SMEM, "staged bf16 tile does not fit in LDS");
-  constexpr int KS = kBK / 16;                 // MFMA K steps per tile
+  constexpr int KS = BK / 16 / KSPLIT;        // MFMA K steps per tile and wavefront
+  static_assert(KS * 16 * KSPLIT == BK, "K split must divide the K slice");
+  static_assert(KSPLIT == 1 || BM * CP * 4 <= AB_BYTES, "K-split partials must fit in LDS");
   constexpr int NMFMA = TM * TN * KS;
   constexpr int NDSR = (TM + TN) * KS;
   constexpr int NDSW = ACH + BCH;
   constexpr int NVMEM = ACH + BCH;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   bf16* As = (bf16*)smem;
-  bf16* Bs = As + 2 * BM * kLdk;
-  constexpr int SPARE = 2 * (BM + BN) * kLdk;  // bf16 index of the spare slot
+  bf16* Bs = As + 2 * BM * LDK;
+  constexpr int SPARE = 2 * (BM + BN) * LDK;  // bf16 index of the spare slot
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
+  // wavefront (kg, wm, wn): sub-tile (wm, wn) over K quarter-slices kg*KS .. kg*KS+KS-1
+  // of every 64-wide K slice
+  const int kg = wave / (WM * WN), wmn = wave - kg * (WM * WN);
+  const int wm = wmn / WN, wn = wmn % WN;
   const int l32 = lane & 31, g = lane >> 5;
   int mt, nt;
   tile_coords((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
@@ -387,7 +392,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
     const int c = tid + i * NT, row = c / CPR;
     const bool in = c < ATOT;
     a_kc[i] = (c % CPR) * 8;
-    a_lds[i] = in ? row * kLdk + a_kc[i] : -1;
+    a_lds[i] = in ? row * LDK + a_kc[i] : -1;
     a_off[i] = (in && m0 + row < a.M) ? ((m0 + row) * a.lda + a_kc[i]) * 2 : kOffOOB;
   }
 #pragma unroll
@@ -395,12 +400,12 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
     const int c = tid + i * NT, row = c / CPR;
     const bool in = c < BTOT;
     b_kc[i] = (c % CPR) * 8;
-    b_lds[i] = in ? row * kLdk + b_kc[i] : -1;
+    b_lds[i] = in ? row * LDK + b_kc[i] : -1;
     b_off[i] = (in && n0 + row < a.N) ? ((n0 + row) * a.ldb + b_kc[i]) * 2 : kOffOOB;
   }
   u32x4 ra[ACH], rb[BCH];
   auto gload = [&](int kt) {
-    const int k0 = kt * kBK;
+    const int k0 = kt * BK;
 #pragma unroll
     for (int i = 0; i < ACH; ++i)
       ra[i] = buffer_load16(ra_src, (k0 + a_kc[i] < a.K && a_off[i] != kOffOOB) ? a_off[i] + 2 * k0 : kOffOOB);
@@ -411,12 +416,12 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
   auto lstore = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
-      const int idx = (ATOT % NT == 0 || a_lds[i] >= 0) ? buf * BM * kLdk + a_lds[i] : SPARE;
+      const int idx = (ATOT % NT == 0 || a_lds[i] >= 0) ? buf * BM * LDK + a_lds[i] : SPARE;
       *(u32x4*)&As[idx] = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
-      const int idx = (BTOT % NT == 0 || b_lds[i] >= 0) ? buf * BN * kLdk + b_lds[i] : SPARE - 2 * BM * kLdk;
+      const int idx = (BTOT % NT == 0 || b_lds[i] >= 0) ? buf * BN * LDK + b_lds[i] : SPARE - 2 * BM * LDK;
       *(u32x4*)&Bs[idx] = rb[i];
     }
   };
@@ -430,21 +435,21 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   auto step = [&](int cur, int kt, bool write_next, bool load_next) {
-    const bf16* Ab = As + cur * BM * kLdk + (wm * TM * 32 + l32) * kLdk + g * 8;
-    const bf16* Bb = Bs + cur * BN * kLdk + (wn * TN * 32 + l32) * kLdk + g * 8;
+    const bf16* Ab = As + cur * BM * LDK + (wm * TM * 32 + l32) * LDK + g * 8 + kg * KS * 16;
+    const bf16* Bb = Bs + cur * BN * LDK + (wn * TN * 32 + l32) * LDK + g * 8 + kg * KS * 16;
     bf16x8 af[2][TM], bfr[2][TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) af[0][i] = *(const bf16x8*)(Ab + i * 32 * kLdk);
+    for (int i = 0; i < TM; ++i) af[0][i] = *(const bf16x8*)(Ab + i * 32 * LDK);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) bfr[0][j] = *(const bf16x8*)(Bb + j * 32 * kLdk);
+    for (int j = 0; j < TN; ++j) bfr[0][j] = *(const bf16x8*)(Bb + j * 32 * LDK);
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       const int cb = kk & 1;
       if (kk + 1 < KS) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) af[cb ^ 1][i] = *(const bf16x8*)(Ab + i * 32 * kLdk + (kk + 1) * 16);
+        for (int i = 0; i < TM; ++i) af[cb ^ 1][i] = *(const bf16x8*)(Ab + i * 32 * LDK + (kk + 1) * 16);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) bfr[cb ^ 1][j] = *(const bf16x8*)(Bb + j * 32 * kLdk + (kk + 1) * 16);
+        for (int j = 0; j < TN; ++j) bfr[cb ^ 1][j] = *(const bf16x8*)(Bb + j * 32 * LDK + (kk + 1) * 16);
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
@@ -470,7 +475,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
     }
   };
 
-  const int nk = (a.K + kBK - 1) / kBK;
+  const int nk = (a.K + BK - 1) / BK;
   gload(0);
   lstore(0);
   if (nk > 1) gload(1);
@@ -491,8 +496,38 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
   // The MFMAs compute C^T blocks (weights as the first operand), so in acc[i][j]
   // lane (l32, g) holds row (wm*TM + i)*32 + l32 of the tile and, in registers
   // 4q..4q+3, the four adjacent columns (wn*TN + j)*32 + 8q + 4g + 0..3.
+  if constexpr (KSPLIT == 2) {
+    // the second K half's partial sums go through LDS to the first half's wavefronts:
+    // one fixed order (first half + second half) for every element
+    float* P = (float*)smem;
+    if (kg == 1) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            *(f32x4*)&P[((wm * TM + i) * 32 + l32) * CP + (wn * TN + j) * 32 + q * 8 + g * 4] = v;
+          }
+    }
+    __syncthreads();
+    if (kg == 0) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = *(const f32x4*)&P[((wm * TM + i) * 32 + l32) * CP + (wn * TN + j) * 32 + q * 8 + g * 4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += v[e];
+          }
+    }
+    __syncthreads();
+  }
   if constexpr (kBf16Out) {
-    bf16_epilogue<KIND, BM, BN, TM, TN, NT>(a, acc, (bf16*)smem, bias_s, m0, n0, wm, wn, l32, g, tid);
+    bf16_epilogue<KIND, BM, BN, TM, TN, NT>(a, acc, (bf16*)smem, bias_s, m0, n0, wm, wn, l32, g, kg == 0, tid);
   } else {
     float* Cs = (float*)smem;
 #pragma unroll
@@ -500,7 +535,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_sched_kernel(GemmArgs 
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int rb0 = (wm * TM + i) * 32;
-        if (rb0 < p * RP || rb0 >= (p + 1) * RP) continue;
+        if (kg != 0 || rb0 < p * RP || rb0 >= (p + 1) * RP) continue;
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -567,18 +602,21 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   }
 }
 
-// Tile shapes (BM x BN, wave grid WM x WN). Per-wave tiles are 64x64 or 64x96.
-#define SF_GEMM_TILES(X)   \
-  X(0, 128, 128, 2, 2)     \
-  X(1, 128, 288, 2, 3)     \
-  X(2, 128, 384, 2, 4)     \
-  X(3, 128, 192, 2, 2)
+// Tile shapes (BM x BN x BK, wave grid WM x WN, K split). Per-wave tiles are 64x64 or
+// 64x96; with a K split of 2 a second set of wavefronts takes the second half of every
+// K slice of the same tile.
+#define SF_GEMM_TILES(X)          \
+  X(0, 128, 128, 64, 2, 2, 1)     \
+  X(1, 128, 288, 64, 2, 3, 1)     \
+  X(2, 128, 384, 64, 2, 4, 1)     \
+  X(3, 128, 192, 64, 2, 2, 1)     \
+  X(6, 128, 128, 128, 2, 2, 2)
 
 struct TileInfo {
   int bm, bn, waves;
 };
 static const TileInfo kTiles[] = {
-#define SF_TILE_INFO(id, bm, bn, wm, wn) {bm, bn, wm * wn},
+#define SF_TILE_INFO(id, bm, bn, bk, wm, wn, ks) {bm, bn, wm * wn * ks},
     SF_GEMM_TILES(SF_TILE_INFO)
 #undef SF_TILE_INFO
 };
@@ -587,10 +625,10 @@ constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 template <EpiKind KIND>
 static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
   switch (tile) {
-#define SF_TILE_CASE(id, bm, bn, wm, wn)                                                   \
-  case id:                                                                                  \
-    launch((gemm_bf16_sched_kernel<bm, bn, wm, wn, KIND>),                      \
-                       dim3(((a.N + bn - 1) / bn) * ((a.M + bm - 1) / bm)), dim3(wm * wn * 64), 0, s, a); \
+#define SF_TILE_CASE(id, bm, bn, bk, wm, wn, ks)                                                   \
+  case id:                                                                                         \
+    launch((gemm_bf16_sched_kernel<bm, bn, bk, wm, wn, ks, KIND>),                                 \
+           dim3(((a.N + bn - 1) / bn) * ((a.M + bm - 1) / bm)), dim3(wm * wn * ks * 64), 0, s, a); \
     break;
     SF_GEMM_TILES(SF_TILE_CASE)
 #undef SF_TILE_CASE
@@ -600,12 +638,20 @@ static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Interleaved tiles, chosen from measurements on the 512^2 and 1024^2 projection
-// shapes: 128x128 (64x64 per wavefront) is the best general tile; 128x384 and 128x288
-// (64x96 per wavefront, 8 and 6 wavefronts) win when they cut the problem into exactly
-// one workgroup per CU (e.g. 4096x3072 and 4096x2304).
+// Tiles chosen from measurements on the 512^2 and 1024^2 projection shapes. Narrow
+// outputs (N <= 1536, e.g. the attention output and MLP down-projections) take 128x128
+// tiles with 128-wide K slices split over two sets of wavefronts: with few output
+// columns there are too few wide tiles to fill the chip, and the second wavefront set
+// keeps the matrix cores fed while loads are in flight. The partial sums of the two
+// halves are added in a fixed order, and the choice depends on N and K only, never on
+// M, so a row's result does not depend on how many rows are in the batch. Otherwise
+// 128x128 (64x64 per wavefront) is the general tile; 128x384 and 128x288 (64x96 per
+// wavefront, 8 and 6 wavefronts) win when they cut the problem into exactly one
+// workgroup per CU (e.g. 4096x3072 and 4096x2304); these three accumulate in the same
+// order, so switching among them with M changes no result bit.
 int choose_gemm_tile(int M, int N, int K) {
   (void)K;
+  if (N % 128 == 0 && N <= 1536) return 6;
   auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
   if (M % 128 == 0 && N % 384 == 0 && tiles(128, 384) == 256) return 2;
   if (M % 128 == 0 && N % 288 == 0 && tiles(128, 288) == 256) return 1;
