@@ -24,12 +24,27 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
   static_assert(RW * kGemvSamples % 16 == 0, "rows x samples must fill butterfly groups");
   const int lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RW;
-  if (j0 >= a.R) return;
+  // the sinusoid mode builds each batch's embedding once per workgroup in LDS (with a
+  // barrier), so there every wavefront stays to the end
+  if (XMODE == 0 && j0 >= a.R) return;
+  __shared__ float emb[XMODE == 1 ? kGemvSamples * kMaxWidth : 1];
   const int nchunk = a.K / E;
   const __amdgpu_buffer_rsrc_t w_src = buffer_rsrc(a.W, (uint32_t)((size_t)a.R * a.K * sizeof(WT)));
   const __amdgpu_buffer_rsrc_t x_src = buffer_rsrc(a.X, a.X ? (uint32_t)((size_t)a.B * a.ldx * 4) : 0u);
   for (int b0 = 0; b0 < a.B; b0 += kGemvSamples) {
     const int nb = min(kGemvSamples, a.B - b0);
+    if constexpr (XMODE == 1) {
+      // [cos | sin] of 1000 t times the frequency table, for this batch's samples
+      const int half = a.K >> 1;
+      __syncthreads();
+      for (int i = threadIdx.x; i < nb * a.K; i += blockDim.x) {
+        const int bb = i / a.K, k = i - bb * a.K;
+        const int f = k < half ? k : k - half;
+        const float phi = (1000.0f * a.t.v[b0 + bb]) * a.freqs[f];
+        emb[i] = k < half ? cosf(phi) : sinf(phi);
+      }
+      __syncthreads();
+    }
     u32x4 w[RW][NC];
 #pragma unroll
     for (int rr = 0; rr < RW; ++rr) {
@@ -48,14 +63,8 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
         const int ch = lane + 64 * c;
         const bool in = bb < nb && ch < nchunk;
         if constexpr (XMODE == 1) {
-          const int half = a.K >> 1;
 #pragma unroll
-          for (int e = 0; e < E; ++e) {
-            const int k = ch * E + e;
-            const int f = k < half ? k : k - half;
-            const float phi = (1000.0f * a.t.v[b0 + min(bb, nb - 1)]) * a.freqs[in ? f : 0];
-            x[bb][c][e] = in ? (k < half ? cosf(phi) : sinf(phi)) : 0.0f;
-          }
+          for (int e = 0; e < E; ++e) x[bb][c][e] = in ? emb[bb * a.K + ch * E + e] : 0.0f;
         } else {
 #pragma unroll
           for (int q = 0; q < E / 4; ++q) {
@@ -144,42 +153,65 @@ hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s) {
   return w_bf16 ? launch_gemv_t<bf16>(a, s) : launch_gemv_t<float>(a, s);
 }
 
-// One thread per four consecutive outputs of one token: the token's p*p*C patch values
+// Patch embedding, h = patches . W_peT + b_pe + pos. The token's p*p*C patch values
 // (feature (i*p + j)*C + c of token gh*(W/p) + gw reads x[c][gh*p + i][gw*p + j]) times
-// the transposed patch-embedding weight W_peT [P][D], plus bias and position row. The
-// 2x2-patch, 4-channel case has every load unrolled and issued up front (eight 8-byte
-// pixel-pair loads and sixteen weight rows); other shapes take the general loop.
+// the transposed patch-embedding weight W_peT [P][D], plus bias and position row.
+//
+// 2x2 patches of 4 channels: a thread owns four adjacent output columns of kEmbedTok
+// consecutive tokens. Its sixteen W_peT rows stay in registers for all of them (the
+// weight is read once per thread instead of once per token), and the lanes of a
+// wavefront share the same tokens, so each pixel-pair load is one broadcast. Tokens are
+// handled in batches of four with every load of a batch issued before its arithmetic.
+constexpr int kEmbedTok = 8;
+
 __global__ __launch_bounds__(256) void embed_p2c4_kernel(EmbedArgs a) {
   const int d4n = a.D >> 2;
+  const int M = a.rows * a.N;
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= a.rows * a.N * d4n) return;
-  const int m = idx / d4n, d = (idx - m * d4n) * 4;
-  const int r = m / a.N;
-  const int n = m - r * a.N;
-  const int lat = r % a.n_lat;
+  const int grp = idx / d4n;
+  const int m0 = grp * kEmbedTok;
+  if (m0 >= M) return;
+  const int d = (idx - grp * d4n) * 4;
   const int gwn = a.W / 2;
-  const int gh = n / gwn, gw = n - gh * gwn;
-  float px[16];
-#pragma unroll
-  for (int c = 0; c < 4; ++c)
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const float2 v = *(const float2*)(a.x + (((size_t)lat * 4 + c) * a.H + gh * 2 + i) * a.W + gw * 2);
-      px[(2 * i + 0) * 4 + c] = v.x;
-      px[(2 * i + 1) * 4 + c] = v.y;
-    }
   float4 w[16];
 #pragma unroll
   for (int f = 0; f < 16; ++f) w[f] = *(const float4*)(a.W_pe + (size_t)f * a.D + d);
   const float4 b = *(const float4*)(a.b_pe + d);
-  const float4 ps = *(const float4*)(a.pos + (size_t)n * a.D + d);
-  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 #pragma unroll
-  for (int f = 0; f < 16; ++f) {
-    acc.x += px[f] * w[f].x; acc.y += px[f] * w[f].y; acc.z += px[f] * w[f].z; acc.w += px[f] * w[f].w;
+  for (int t0 = 0; t0 < kEmbedTok; t0 += 4) {
+    float px[4][16];
+    float4 ps[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int m = min(m0 + t0 + t, M - 1);
+      const int r = m / a.N;
+      const int n = m - r * a.N;
+      const int lat = r % a.n_lat;
+      const int gh = n / gwn, gw = n - gh * gwn;
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const float2 v = *(const float2*)(a.x + (((size_t)lat * 4 + c) * a.H + gh * 2 + i) * a.W + gw * 2);
+          px[t][(2 * i + 0) * 4 + c] = v.x;
+          px[t][(2 * i + 1) * 4 + c] = v.y;
+        }
+      ps[t] = *(const float4*)(a.pos + (size_t)n * a.D + d);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int m = m0 + t0 + t;
+      float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+      for (int f = 0; f < 16; ++f) {
+        acc.x += px[t][f] * w[f].x; acc.y += px[t][f] * w[f].y;
+        acc.z += px[t][f] * w[f].z; acc.w += px[t][f] * w[f].w;
+      }
+      if (m < M)
+        *(float4*)(a.h + (size_t)m * a.D + d) = make_float4((acc.x + b.x) + ps[t].x, (acc.y + b.y) + ps[t].y,
+                                                            (acc.z + b.z) + ps[t].z, (acc.w + b.w) + ps[t].w);
+    }
   }
-  *(float4*)(a.h + (size_t)m * a.D + d) =
-      make_float4((acc.x + b.x) + ps.x, (acc.y + b.y) + ps.y, (acc.z + b.z) + ps.z, (acc.w + b.w) + ps.w);
 }
 
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
@@ -209,10 +241,12 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   const int total = a.rows * a.N * (a.D >> 2);
-  if (a.p == 2 && a.C == 4)
-    launch(embed_p2c4_kernel, dim3((total + 255) / 256), dim3(256), 0, s, a);
-  else
+  if (a.p == 2 && a.C == 4) {
+    const int threads = (a.rows * a.N + kEmbedTok - 1) / kEmbedTok * (a.D >> 2);
+    launch(embed_p2c4_kernel, dim3((threads + 255) / 256), dim3(256), 0, s, a);
+  } else {
     launch(embed_kernel, dim3((total + 255) / 256), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
