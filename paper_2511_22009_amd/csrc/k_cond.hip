@@ -160,9 +160,9 @@ hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s) {
 // 2x2 patches of 4 channels: a thread owns four adjacent output columns of kEmbedTok
 // consecutive tokens. Its sixteen W_peT rows stay in registers for all of them (the
 // weight is read once per thread instead of once per token), and the lanes of a
-// wavefront share the same tokens, so each pixel-pair load is one broadcast. Tokens are
-// handled in batches of four with every load of a batch issued before its arithmetic.
-constexpr int kEmbedTok = 8;
+// wavefront share the same tokens, so each pixel-pair load is one broadcast. Every load
+// of a batch of four tokens is issued before its arithmetic.
+constexpr int kEmbedTok = 4;
 
 __global__ __launch_bounds__(256) void embed_p2c4_kernel(EmbedArgs a) {
   const int d4n = a.D >> 2;
