@@ -29,41 +29,24 @@ constexpr int kKH = 32;    // keys per half per step
 constexpr int kQB = 64;    // queries per workgroup
 constexpr float kLazy = 8.0f;  // max drift (exp2 units) tolerated before a rescale
 
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-// Combine a value with the one lane l ^ 32 holds: v_permlane32_swap exchanges the two
-// 32-lane halves of its operands, so with both operands v every lane gets its own value
-// in one result and its partner's in the other. max and + are symmetric, so both lanes
-// of a pair get the same bits, without a trip through LDS.
-__device__ __forceinline__ float half_max(float v) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float half_sum(float v) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 template <int DHC, int DB>  // DHC = ceil(dh/16) contraction chunks, DB = ceil(dh/32) dh blocks
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DB <= 2 ? 3 : 2))) void attn_bf16_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   constexpr int KLD = DHC * 16 + 8;     // K tile row pitch (bf16)
   constexpr int VLD = kKH + 8;          // V^T tile row pitch (bf16)
   constexpr int VROWS = DB * 32;
   constexpr int KT = kKH * KLD;         // one half's K tile (bf16 elements)
   constexpr int VT = VROWS * VLD;       // one half's V^T tile
-  constexpr int NKB = 3, NVB = 2;       // ring depths of the K and V^T step tiles
   constexpr int KCHMAX = 2 * kKH * DHC * 2;        // 16-byte K chunks per step (upper bound)
   constexpr int VCHMAX = VROWS * (2 * kKH / 8);    // 16-byte V^T chunks per step (upper bound)
   constexpr int KCH = (KCHMAX + 255) / 256;
   constexpr int VCH = (VCHMAX + 255) / 256;
-  constexpr int TILE_BYTES = (NKB * 2 * KT + NVB * 2 * VT) * 2;
+  constexpr int TILE_BYTES = 2 * 2 * (KT + VT) * 2;             // [buf][half] K and V^T
   constexpr int MERGE_BYTES = 2 * 64 * (DB * 16 + 2) * 4;       // per query group: o, m, l
-  constexpr int BODY = TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES;
-  constexpr int SMEM = BODY + 16;                                // + spare slot
+  constexpr int SMEM = (TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) + 16;  // + spare slot
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  bf16* const Ks = (bf16*)smem;                  // [NKB][half][kKH][KLD]
-  bf16* const Vs = Ks + NKB * 2 * KT;            // [NVB][half][VROWS][VLD]
-  constexpr int SPARE = BODY / 2;                // bf16 index of the spare slot
+  bf16* const Ks = (bf16*)smem;                  // [buf][half][kKH][KLD]
+  bf16* const Vs = Ks + 2 * 2 * KT;              // [buf][half][VROWS][VLD]
+  const int SPARE = (TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) / 2;  // bf16 index
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qg = wave & 1, kh = wave >> 1;
@@ -127,28 +110,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DB <= 2 ? 3
     v_lds[i] = in ? (kg >> 2) * VT + d * VLD + (kg & 3) * 8 : -1;
   }
   u32x4 rk[KCH], rv[VCH];
-  auto gload_k = [&](int step) {
-    const int kv0 = step * 2 * kKH;
+  auto gload = [&](int kv0) {
 #pragma unroll
     for (int i = 0; i < KCH; ++i)
       rk[i] = buffer_load16(k_src, kv0 + k_key[i] < a.Nk ? k_goff[i] + kv0 * dh * 2 : kOffOOB);
-  };
-  auto gload_v = [&](int step) {
-    const int kv0 = step * 2 * kKH;
 #pragma unroll
     for (int i = 0; i < VCH; ++i)
       rv[i] = buffer_load16(v_src, kv0 + v_key[i] < a.ldv ? v_goff[i] + kv0 * 2 : kOffOOB);
   };
-  // the chunk counts depend on dh at run time, so every chunk checks its slot
-  auto lstore_k = [&](int slot) {
+  auto lstore = [&](int buf) {
+    // the chunk counts depend on dh at run time, so every chunk checks its slot
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) *(u32x4*)&Ks[k_lds[i] >= 0 ? slot * 2 * KT + k_lds[i] : SPARE] = rk[i];
-  };
-  auto lstore_v = [&](int slot) {
+    for (int i = 0; i < KCH; ++i) *(u32x4*)&Ks[k_lds[i] >= 0 ? buf * 2 * KT + k_lds[i] : SPARE] = rk[i];
 #pragma unroll
-    for (int i = 0; i < VCH; ++i)
-      *(u32x4*)&Vs[v_lds[i] >= 0 ? slot * 2 * VT + v_lds[i] : SPARE - NKB * 2 * KT] = rv[i];
+    for (int i = 0; i < VCH; ++i) *(u32x4*)&Vs[v_lds[i] >= 0 ? buf * 2 * VT + v_lds[i] : SPARE - 4 * KT] = rv[i];
   };
+
   f32x16 o[DB];
 #pragma unroll
   for (int b = 0; b < DB; ++b)
@@ -156,56 +133,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DB <= 2 ? 3
     for (int e = 0; e < 16; ++e) o[b][e] = 0.0f;
   float m2 = -INFINITY, lsum = 0.0f;               // running max in exp2 units, partial sum
   const float sl2 = a.scale * 1.4426950408889634f;  // scores -> exp2 units
-  const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
 
-  // raw scores S^T = K Q^T from K slot `slot` into s: s[e] is query l32 and key
-  // step*64 + kh*32 + (e/4)*8 + g*4 + e%4
-  auto scores = [&](const bf16x8 (&kf)[DHC], f32x16& s) {
+  const int nsteps = (a.Nk + 2 * kKH - 1) / (2 * kKH);
+  __syncthreads();
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int it = 0; it < nsteps; ++it) {
+    const int cur = it & 1;
+    const int kv0 = it * 2 * kKH + kh * kKH;      // this wavefront's first key
+    if (it + 1 < nsteps) gload((it + 1) * 2 * kKH);
+    const bf16* Kb = Ks + (cur * 2 + kh) * KT;
+    const bf16* Vb = Vs + (cur * 2 + kh) * VT;
+
+    f32x16 s;
 #pragma unroll
     for (int e = 0; e < 16; ++e) s[e] = 0.0f;
 #pragma unroll
-    for (int kk = 0; kk < DHC; ++kk) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], s, 0, 0, 0);
-  };
-  auto kfrags = [&](int slot, bf16x8 (&kf)[DHC]) {
-    const bf16* Kb = Ks + (slot * 2 + kh) * KT;
-#pragma unroll
-    for (int kk = 0; kk < DHC; ++kk) kf[kk] = *(const bf16x8*)&Kb[l32 * KLD + kk * 16 + g * 8];
-  };
-
-  // Software pipeline: the scores of step j+1 are issued on the matrix cores in the same
-  // block as the softmax of step j on the vector ALUs, so the two overlap inside a
-  // wavefront, and every LDS fragment read of a step is issued at its top. K slots
-  // rotate over three buffers and V^T over two, so the one barrier per step covers
-  // every hazard: step j reads K slot (j+1)%3 and V slot j%2, and writes K of step j+2
-  // to slot (j+2)%3 and V of step j+1 to slot (j+1)%2, whose previous contents were
-  // last read before the barrier that ended step j-1.
-  const int nsteps = (a.Nk + 2 * kKH - 1) / (2 * kKH);
-  auto step = [&](f32x16& s, f32x16& sn, int it) {
-    const int kv0 = it * 2 * kKH + kh * kKH;      // this wavefront's first key
-    bf16x8 kf[DHC];
-    kfrags((it + 1) % NKB, kf);                   // stale at the last step: those scores are unused
-    bf16x8 vf[DB][2];
-    const bf16* Vb = Vs + ((it % NVB) * 2 + kh) * VT;
-#pragma unroll
-    for (int b = 0; b < DB; ++b)
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const bf16* vr = &Vb[(b * 32 + l32) * VLD + ks * 16 + g * 4];
-        const bf16x4 lo = *(const bf16x4*)vr;
-        const bf16x4 hi = *(const bf16x4*)(vr + 8);
-        vf[b][ks] = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-      }
-    // only the last, ragged step needs the key mask
+    for (int kk = 0; kk < DHC; ++kk) {
+      const bf16x8 kf = *(const bf16x8*)&Kb[l32 * KLD + kk * 16 + g * 8];
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
+    }
+    // s[e]: query l32, key kv0 + (e/4)*8 + g*4 + e%4, raw (unscaled). Only the last,
+    // ragged step needs the key mask.
     if (kv0 + kKH > a.Nk) {
 #pragma unroll
       for (int e = 0; e < 16; ++e)
         if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) s[e] = -INFINITY;
     }
-    // max over the 32 keys of the query: 16 here, 16 in lane l ^ 32
     float tmax = s[0];
 #pragma unroll
     for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, s[e]);
-    tmax = half_max(tmax) * sl2;
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
     if (__any(tmax > m2 + kLazy)) {
       const float mnew = fmaxf(m2, tmax);
       const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
@@ -216,56 +175,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DB <= 2 ? 3
         for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
       m2 = mnew;
     }
-    scores(kf, sn);
     bf16x8 pf[2];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) pf[ks][j] = (bf16)__builtin_amdgcn_exp2f(fmaf(s[ks * 8 + j], sl2, -m2));
-      // the row sum takes the rounded probabilities, the same ones that weight V
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[ks][2 * j], pf[ks][2 * j + 1]}, ones, lsum, false);
+      for (int j = 0; j < 8; ++j) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[ks * 8 + j], sl2, -m2));
+        lsum += p;
+        pf[ks][j] = (bf16)p;
+      }
     }
 #pragma unroll
-    for (int b = 0; b < DB; ++b)
+    for (int b = 0; b < DB; ++b) {
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[b][ks], pf[ks], o[b], 0, 0, 0);
-    // the next step's score MFMAs between this step's exp work
-#pragma unroll
-    for (int kk = 0; kk < DHC; ++kk) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16* vr = &Vb[(b * 32 + l32) * VLD + ks * 16 + g * 4];
+        const bf16x4 lo = *(const bf16x4*)vr;
+        const bf16x4 hi = *(const bf16x4*)(vr + 8);
+        const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
+      }
     }
-    if (it + 2 < nsteps) lstore_k((it + 2) % NKB);
-    if (it + 1 < nsteps) lstore_v((it + 1) % NVB);
-    if (it + 3 < nsteps) gload_k(it + 3);
-    if (it + 2 < nsteps) gload_v(it + 2);
+    if (it + 1 < nsteps) lstore(cur ^ 1);
     __syncthreads();
-  };
-
-  __syncthreads();
-  gload_k(0);
-  gload_v(0);
-  lstore_k(0);
-  lstore_v(0);
-  gload_k(1);
-  lstore_k(1);
-  gload_k(2);
-  gload_v(1);
-  __syncthreads();
-  f32x16 sa, sb;
-  {
-    bf16x8 kf[DHC];
-    kfrags(0, kf);
-    scores(kf, sa);
   }
-  int it = 0;
-  for (; it + 1 < nsteps; it += 2) {
-    step(sa, sb, it);
-    step(sb, sa, it + 1);
-  }
-  if (it < nsteps) step(sa, sb, it);
 
   // merge the key halves: half 1 hands (o, max, partial sum) to half 0 through LDS
   float* mg = (float*)smem + qg * 64 * (DB * 16 + 2);
@@ -284,7 +217,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DB <= 2 ? 3
   const float a0 = m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2 - mnew);
   const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
   lsum = lsum * a0 + mg[(DB * 16 + 1) * 64 + lane] * a1;
-  lsum = half_sum(lsum);
+  lsum += __shfl_xor(lsum, 32);
   const float inv = 1.0f / lsum;
   if (qi < a.Nq) {
     bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi) * a.D + (size_t)head * dh;
