@@ -639,10 +639,12 @@ static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
 }
 
 // Tiles chosen from measurements on the 512^2 and 1024^2 projection shapes. Narrow
-// outputs (N <= 1536, e.g. the attention output and MLP down-projections) take 128x128
-// tiles with 128-wide K slices split over two sets of wavefronts: with few output
-// columns there are too few wide tiles to fill the chip, and the second wavefront set
-// keeps the matrix cores fed while loads are in flight. The partial sums of the two
+// outputs (N <= 768, e.g. the attention output and MLP down-projections of the width-768
+// network) take 128x128 tiles with 128-wide K slices split over two sets of wavefronts:
+// with few output columns there are too few wide tiles to fill the chip, and the second
+// wavefront set keeps the matrix cores fed while loads are in flight. (At N = 1152 the
+// 128x128 tiles outnumber the CUs, and the split tile, one workgroup per CU, loses to
+// the plain one, two per CU: 72 vs 67 us on 4096x1152x4608.) The partial sums of the two
 // halves are added in a fixed order, and the choice depends on N and K only, never on
 // M, so a row's result does not depend on how many rows are in the batch. Otherwise
 // 128x128 (64x64 per wavefront) is the general tile; 128x384 and 128x288 (64x96 per
@@ -651,7 +653,7 @@ static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
 // order, so switching among them with M changes no result bit.
 int choose_gemm_tile(int M, int N, int K) {
   (void)K;
-  if (N % 128 == 0 && N <= 1536) return 6;
+  if (N % 128 == 0 && N <= 768) return 6;
   auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
   if (M % 128 == 0 && N % 384 == 0 && tiles(128, 384) == 256) return 2;
   if (M % 128 == 0 && N % 288 == 0 && tiles(128, 288) == 256) return 1;
