@@ -609,7 +609,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   X(0, 128, 128, 64, 2, 2, 1)     \
   X(1, 128, 288, 64, 2, 3, 1)     \
   X(2, 128, 384, 64, 2, 4, 1)     \
-  X(3, 128, 192, 64, 2, 2, 1)     \
   X(6, 128, 128, 128, 2, 2, 2)
 
 struct TileInfo {

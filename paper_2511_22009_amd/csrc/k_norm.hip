@@ -104,7 +104,9 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
 
 template <typename OT, int NV>
 static void launch_ln_nv(const LnArgs& a, hipStream_t s) {
-  constexpr int RPW = NV <= 4 ? 2 : 1;
+  // one row per wavefront: more wavefronts in flight beat more rows per wavefront
+  // (4096 x 768: 4.5 us against 5.1 us with two rows)
+  constexpr int RPW = 1;
   const int grid = (a.M + 4 * RPW - 1) / (4 * RPW);
   launch((ln_mod_kernel<OT, NV, RPW>), dim3(grid), dim3(256), 0, s, a);
 }
