@@ -7,8 +7,9 @@
 //   GELU     out = GELU_tanh(acc + bias);
 //   RES      h += acc + bias.
 //
-// bf16 path: v_mfma_f32_32x32x16_bf16 on BM x BN x 64 workgroup tiles (table at the
-// end), each wavefront owning a 64x64 or 64x96 sub-tile; both operand tiles are
+// bf16 path: v_mfma_f32_32x32x16_bf16 on BM x BN x BK workgroup tiles (BK 64 or 128;
+// table at the end), each wavefront owning a 64x64 or 64x96 sub-tile, optionally with
+// the K slice split over two sets of wavefronts; both operand tiles are
 // double-buffered in LDS with a 16-byte row pad so the 16-byte fragment reads of a
 // 32-lane column are free of bank conflicts, and the next K-slice is fetched into
 // registers while the current one feeds the matrix cores. The MFMAs take the weight
@@ -57,11 +58,6 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int m, int n, float 
 
 // ------------------------------------------------------------------ bf16 / MFMA
 
-__device__ __forceinline__ void store4(bf16* p, float a, float b, float c, float d) {
-  const bf16x4 v = {(bf16)a, (bf16)b, (bf16)c, (bf16)d};
-  *(bf16x4*)p = v;
-}
-
 // Largest divisor of n that is at most cap: the number of epilogue items a thread
 // handles per batch.
 constexpr int batch_of(int n, int cap) {
@@ -70,16 +66,16 @@ constexpr int batch_of(int n, int cap) {
   return 1;
 }
 
-// Epilogue over the C tile staged in LDS (fp32, row pitch CP), four outputs per
-// item: row-contiguous for h, GELU output, q and k; token-contiguous for the
-// transposed v. Items are processed in batches: every load of a batch (C from LDS,
-// bias, gate, residual) is issued before any of its results is used, with out-of-tile
-// items reading a clamped in-range address, so a batch pays one memory latency
-// instead of one per item. Only the stores are predicated.
+// Epilogue of the fp32 residual projections (h += gate[sample] * (acc + bias) and
+// h += acc + bias) over the C tile staged in LDS (fp32, row pitch CP), four adjacent
+// outputs of a row per item. Items are processed in batches: every load of a batch (C
+// from LDS, bias, gate, residual) is issued before any of its results is used, with
+// out-of-tile items reading a clamped in-range address, so a batch pays one memory
+// latency instead of one per item. Only the stores are predicated.
 template <EpiKind KIND, int BM, int BN, int NT>
 __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const float* Cs, int CP, int m0, int n0,
                                                 int tid) {
-  constexpr bool kRes = KIND == EPI_RES || KIND == EPI_RES_GATE || KIND == EPI_RES_GATE_MLP;
+  static_assert(KIND == EPI_RES || KIND == EPI_RES_GATE || KIND == EPI_RES_GATE_MLP, "residual epilogues only");
   constexpr bool kGate = KIND == EPI_RES_GATE || KIND == EPI_RES_GATE_MLP;
   constexpr int C4 = BN / 4;
   constexpr int TOTAL = BM * C4;
@@ -99,7 +95,7 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const float* 
       nn[u] = ok[u] ? n : 0;
       cv[u] = *(const float4*)&Cs[(ok[u] ? row : 0) * CP + (ok[u] ? c4 * 4 : 0)];
       bv[u] = *(const float4*)(a.bias + nn[u]);
-      if constexpr (kRes) hv[u] = *(const float4*)(a.h + (size_t)mm[u] * a.ldh + nn[u]);
+      hv[u] = *(const float4*)(a.h + (size_t)mm[u] * a.ldh + nn[u]);
       if constexpr (kGate) {
         const int r = (int)fdiv((uint32_t)mm[u], a.div_ntok);
         const int slot = r < a.n_slots ? r : r - a.n_slots;
@@ -110,80 +106,13 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const float* 
     for (int u = 0; u < U; ++u) {
       const int m = mm[u], n = nn[u];
       const float v0 = cv[u].x + bv[u].x, v1 = cv[u].y + bv[u].y, v2 = cv[u].z + bv[u].z, v3 = cv[u].w + bv[u].w;
-      if constexpr (KIND == EPI_QKV) {
-        const int part = (int)fdiv((uint32_t)n, a.div_D);
-        const int which = a.which_base + part;
-        const int rem = n - part * a.D;
-        const int head = (int)fdiv((uint32_t)rem, a.div_dh);
-        const int d = rem - head * a.dh;
-        const int r = (int)fdiv((uint32_t)m, a.div_ntok);
-        const int tok = m - r * a.ntok;
-        bf16* base = (bf16*)(which == 0 ? a.q : a.k);
-        if (ok[u] && which < 2)  // v columns: second pass
-          store4(base + (((size_t)r * a.heads + head) * a.ntok + tok) * a.dh + d, v0, v1, v2, v3);
-      } else if constexpr (kGate) {
-        float4 h = hv[u];
+      float4 h = hv[u];
+      if constexpr (kGate) {
         h.x += gv[u].x * v0; h.y += gv[u].y * v1; h.z += gv[u].z * v2; h.w += gv[u].w * v3;
-        if (ok[u]) *(float4*)(a.h + (size_t)m * a.ldh + n) = h;
-      } else if constexpr (KIND == EPI_GELU) {
-        const float o0 = gelu_tanh(v0), o1 = gelu_tanh(v1), o2 = gelu_tanh(v2), o3 = gelu_tanh(v3);
-        if (ok[u]) store4((bf16*)a.out + (size_t)m * a.ldo + n, o0, o1, o2, o3);
       } else {
-        float4 h = hv[u];
         h.x += v0; h.y += v1; h.z += v2; h.w += v3;
-        if (ok[u]) *(float4*)(a.h + (size_t)m * a.ldh + n) = h;
       }
-    }
-  }
-  if constexpr (KIND == EPI_QKV) {
-    // transposed v: item = (column, 4 consecutive rows); skipped unless the tile
-    // reaches the v columns
-    if (a.which_base + (int)fdiv((uint32_t)min(n0 + BN, a.N) - 1, a.div_D) < 2) return;
-    constexpr int R4 = BM / 4;
-    constexpr int VT = R4 * BN;
-    constexpr int VIT = (VT + NT - 1) / NT;
-    constexpr int VU = batch_of(VIT, 8);
-    for (int i0 = 0; i0 < VIT; i0 += VU) {
-      float cq[VU][4], bq[VU];
-      int col_[VU], r4_[VU];
-      bool ok[VU];
-#pragma unroll
-      for (int u = 0; u < VU; ++u) {
-        const int c = tid + (i0 + u) * NT;
-        const int col = c / R4, r4 = c - col * R4;
-        const int n = n0 + col, m = m0 + r4 * 4;
-        const bool in = (VT % NT == 0 || c < VT) && n < a.N && m < a.M;
-        ok[u] = in && a.which_base + (int)fdiv((uint32_t)n, a.div_D) >= 2;
-        col_[u] = ok[u] ? col : 0;
-        r4_[u] = ok[u] ? r4 : 0;
-        const float* cp = Cs + (r4_[u] * 4) * CP + col_[u];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) cq[u][q] = cp[q * CP];
-        bq[u] = a.bias[n0 + col_[u]];
-      }
-#pragma unroll
-      for (int u = 0; u < VU; ++u) {
-        if (!ok[u]) continue;
-        const int n = n0 + col_[u], m = m0 + r4_[u] * 4;
-        const int part = (int)fdiv((uint32_t)n, a.div_D);
-        const int rem = n - part * a.D;
-        const int head = (int)fdiv((uint32_t)rem, a.div_dh);
-        const int d = rem - head * a.dh;
-        const int r = (int)fdiv((uint32_t)m, a.div_ntok);
-        const int tok = m - r * a.ntok;
-        bf16* vt = (bf16*)a.vT + (((size_t)r * a.heads + head) * a.dh + d) * a.ldv;
-        const float bn = bq[u];
-        if (tok + 3 < a.ntok && m + 3 < a.M && (tok & 3) == 0) {
-          store4(vt + tok, cq[u][0] + bn, cq[u][1] + bn, cq[u][2] + bn, cq[u][3] + bn);
-        } else {
-          for (int q = 0; q < 4 && m + q < a.M; ++q) {
-            const int mq = m + q;
-            const int rq = (int)fdiv((uint32_t)mq, a.div_ntok);
-            const int tq = mq - rq * a.ntok;
-            ((bf16*)a.vT)[(((size_t)rq * a.heads + head) * a.dh + d) * a.ldv + tq] = (bf16)(cq[u][q] + bn);
-          }
-        }
-      }
+      if (ok[u]) *(float4*)(a.h + (size_t)m * a.ldh + n) = h;
     }
   }
 }
