@@ -480,6 +480,296 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
   }
 }
 
+// ------------------------------------------------- bf16 / MFMA, direct LDS staging
+//
+// The same tile computation with operand slices moved by buffer_load ... lds straight
+// from global memory into a ring of STAGES LDS buffers (no VGPR round trip, no LDS
+// write instructions), fetched STAGES - 1 slices ahead.
+//
+// Each stage is its own __shared__ variable and the main loop is unrolled by STAGES, so
+// every LDS access names one variable: the compiler then tells the in-flight loads into
+// other stages apart from the stage being read and waits only for the right ones.
+// The loop's barrier is a bare s_barrier (ordered by compiler-only fences) after an
+// explicit wait for this slice's loads: the workgroup-scope release fence of
+// __syncthreads would wait for every outstanding LDS-bound load, i.e. for all stages.
+//
+// Stage layout: rows of BK bf16 without padding; 16-byte chunk c of row r sits at chunk
+// position c ^ swz(r), which keeps the fragment reads (one row per lane, lanes 0-15 and
+// 16-31 each reading one chunk column of 16 consecutive rows) free of bank conflicts
+// whether the LDS serves 8 or 16 lanes of a 16-byte read per cycle.
+template <int CPR>
+__device__ __forceinline__ int dma_swz(int r) {
+  static_assert(CPR == 8 || CPR == 16, "8 or 16 chunks per row");
+  if constexpr (CPR == 8)
+    return (r & 7) ^ ((r >> 3) & 1);
+  else
+    return r & 15;
+}
+
+// A non-template wrapper: with the builtin written inside the kernel template the
+// host-side pass of this compiler dropped the kernels' launch stubs.
+__device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, char* lds, int off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
+}
+
+// Workgroup barrier without a memory fence; the signal fences keep the compiler from
+// moving LDS accesses across it. Callers wait for what the barrier must cover first.
+__device__ __forceinline__ void bare_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+template <int N>
+__device__ __forceinline__ constexpr int waitcnt_vm_only() {
+  static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
+  return (N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8);
+}
+template <int N>
+__device__ __forceinline__ constexpr int waitcnt_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
+  return (N & 15) | ((N >> 4) << 14) | (7 << 4);
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int KSPLIT, int STAGES, EpiKind KIND>
+__global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(GemmArgs a) {
+  constexpr int NT = WM * WN * KSPLIT * 64;
+  constexpr int TM = BM / WM / 32;
+  constexpr int TN = BN / WN / 32;
+  static_assert(TM * WM * 32 == BM && TN * WN * 32 == BN, "wave grid must tile the block");
+  constexpr int CPR = BK / 8;
+  constexpr int ATOT = BM * CPR, BTOT = BN * CPR;
+  static_assert(ATOT % 64 == 0 && BTOT % 64 == 0, "whole wavefronts of 16-byte chunks per slice");
+  constexpr int ACH = (ATOT + NT - 1) / NT, BCH = (BTOT + NT - 1) / NT, LPT = ACH + BCH;
+  constexpr int KS = BK / 16 / KSPLIT;  // MFMA K steps per slice and wavefront
+  static_assert(KS * 16 * KSPLIT == BK, "K split must divide the K slice");
+  static_assert(STAGES == 3 || STAGES == 4, "three or four stages");
+  constexpr bool kBf16Out = KIND == EPI_GELU || KIND == EPI_QKV;
+  // each stage buffer also holds, after the main loop, one row block of the K-split
+  // partial sums, one half of the fp32 output tile, or the whole bf16 output tile
+  constexpr int CP = BN + 4;
+  constexpr int RP = BM / 2;
+  constexpr int SLICE = (BM + BN) * BK * 2;
+  // K-split partials: MFMA block b = i * TN + j of every first-set wavefront (4 KB each)
+  // goes to stage b % STAGES at block slot b / STAGES
+  constexpr int PBLK = WM * WN * 16 * 64 * 4;
+  constexpr int PART = KSPLIT == 2 ? (TM * TN + STAGES - 1) / STAGES * PBLK : 0;
+  constexpr int EPI = kBf16Out ? BM * (BN + kEpiPad) * 2 : RP * CP * 4;
+  constexpr int SBA = SLICE > PART ? (SLICE > EPI ? SLICE : EPI) : (PART > EPI ? PART : EPI);
+  static_assert(KSPLIT == 1 || KSPLIT == 2, "K split of one or two");
+  static_assert(STAGES * SBA + (kBf16Out ? BN * 4 : 16) <= 160 * 1024, "stages do not fit in LDS");
+  constexpr int NMFMA = TM * TN * KS;
+  constexpr int NDSR = (TM + TN) * KS;
+  __shared__ __attribute__((aligned(16))) char st0[SBA];
+  __shared__ __attribute__((aligned(16))) char st1[SBA];
+  __shared__ __attribute__((aligned(16))) char st2[SBA];
+  __shared__ __attribute__((aligned(16))) char st3[STAGES > 3 ? SBA : 16];
+  // destination of the loads of wavefronts whose chunk round lies past the tile (they
+  // read zeros; nothing reads this back)
+  constexpr bool kSpare = ATOT % NT != 0 || BTOT % NT != 0;
+  __shared__ __attribute__((aligned(16))) char spare[kSpare ? 1024 : 16];
+  auto stage = [&](auto s) -> char* {
+    constexpr int S = decltype(s)::value % STAGES;
+    if constexpr (S == 0) return st0;
+    else if constexpr (S == 1) return st1;
+    else if constexpr (S == 2) return st2;
+    else return st3;
+  };
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int kg = wave / (WM * WN), wmn = wave - kg * (WM * WN);
+  const int wm = wmn / WN, wn = wmn % WN;
+  const int l32 = lane & 31, g = lane >> 5;
+  int mt, nt;
+  tile_coords((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
+  __shared__ __attribute__((aligned(16))) float bias_s[kBf16Out ? BN : 4];
+  if constexpr (kBf16Out) {
+    for (int c = tid; c < BN / 4; c += NT) {
+      const int n = n0 + 4 * c;
+      *(f32x4*)&bias_s[4 * c] = n < a.N ? *(const f32x4*)(a.bias + n) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+
+  const __amdgpu_buffer_rsrc_t ra_src = buffer_rsrc(a.A, (uint32_t)a.M * a.lda * 2);
+  const __amdgpu_buffer_rsrc_t rb_src = buffer_rsrc(a.B, (uint32_t)a.N * a.ldb * 2);
+  // load i of a thread fills LDS chunk position i * NT + tid of the A (or B) part of a
+  // stage, i.e. tile row p / CPR at chunk position p % CPR, which holds K chunk
+  // (p % CPR) ^ swz(row); per load: that K column and the byte offset at k = 0
+  int a_off[ACH], b_off[BCH], a_kc[ACH], b_kc[BCH];
+#pragma unroll
+  for (int i = 0; i < ACH; ++i) {
+    const int p = tid + i * NT, row = p / CPR;
+    a_kc[i] = ((p % CPR) ^ dma_swz<CPR>(row)) * 8;
+    a_off[i] = p < ATOT && m0 + row < a.M ? ((m0 + row) * a.lda + a_kc[i]) * 2 : kOffOOB;
+  }
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) {
+    const int p = tid + i * NT, row = p / CPR;
+    b_kc[i] = ((p % CPR) ^ dma_swz<CPR>(row)) * 8;
+    b_off[i] = p < BTOT && n0 + row < a.N ? ((n0 + row) * a.ldb + b_kc[i]) * 2 : kOffOOB;
+  }
+  // slice kt into stage buffer sb: every thread issues exactly LPT loads (past the end
+  // of K they read zeros), each wavefront's 64 lanes filling one contiguous kilobyte
+  auto issue = [&](char* sb, int kt) {
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int i = 0; i < ACH; ++i) {
+      const bool in = ATOT % NT == 0 || i * NT + wave * 64 < ATOT;
+      buffer_load16_lds(ra_src, in ? sb + (i * NT + wave * 64) * 16 : spare,
+                        (k0 + a_kc[i] < a.K && a_off[i] != kOffOOB) ? a_off[i] + 2 * k0 : kOffOOB);
+    }
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      const bool in = BTOT % NT == 0 || i * NT + wave * 64 < BTOT;
+      buffer_load16_lds(rb_src, in ? sb + ATOT * 16 + (i * NT + wave * 64) * 16 : spare,
+                        (k0 + b_kc[i] < a.K && b_off[i] != kOffOOB) ? b_off[i] + 2 * k0 : kOffOOB);
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  // this lane's rows all have the swizzle of row l32 (row blocks are 32 apart); its
+  // fragment of MFMA K step kk is K chunk c0 + 2 kk
+  const int sw = dma_swz<CPR>(l32);
+  const int c0 = 2 * kg * KS + g;
+  const int a_row = (wm * TM * 32 + l32) * CPR;
+  const int b_row = ATOT + (wn * TN * 32 + l32) * CPR;
+  // one K slice: wait for this slice's loads (the later slices' STAGES - 2 stay in
+  // flight) and for this thread's LDS accesses, barrier, then the MFMAs on stage S
+  // interleaved with the fragment reads and with the loads of slice kt + STAGES - 1
+  // into the stage read in the previous step
+  constexpr int kWait = waitcnt_vm_lgkm0<(STAGES - 2) * LPT>();
+  auto step = [&](auto s, int kt) {
+    constexpr int S = decltype(s)::value;
+    __builtin_amdgcn_s_waitcnt(kWait);
+    bare_barrier();
+    const char* cur = stage(std::integral_constant<int, S>{});
+    bf16x8 af[2][TM], bfr[2][TN];
+    auto frag = [&](int row_base, int blk, int kk) {
+      return *(const bf16x8*)(cur + (row_base + blk * 32 * CPR + ((c0 + 2 * kk) ^ sw)) * 16);
+    };
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[0][i] = frag(a_row, i, 0);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bfr[0][j] = frag(b_row, j, 0);
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int cb = kk & 1;
+      if (kk + 1 < KS) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) af[cb ^ 1][i] = frag(a_row, i, kk + 1);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) bfr[cb ^ 1][j] = frag(b_row, j, kk + 1);
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cb][j], af[cb][i], acc[i][j], 0, 0, 0);
+    }
+    issue(stage(std::integral_constant<int, S + STAGES - 1>{}), kt + STAGES - 1);
+    constexpr int H1 = NMFMA / 2, H2 = NMFMA - NMFMA / 2;
+#pragma unroll
+    for (int i = 0; i < H1; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, (NDSR + H1 - 1) / H1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < H2; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x020, (LPT + H2 - 1) / H2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+  };
+
+  const int nk = (a.K + BK - 1) / BK;
+  issue(stage(std::integral_constant<int, 0>{}), 0);
+  issue(stage(std::integral_constant<int, 1>{}), 1);
+  if constexpr (STAGES > 3) issue(stage(std::integral_constant<int, 2>{}), 2);
+  // whole rounds of STAGES steps in a loop with one exit (early exits inside the round
+  // would give the loop header a path on which the stage it reads was just issued),
+  // then the remaining steps
+  int kt = 0;
+  for (; kt + STAGES <= nk; kt += STAGES) {
+    step(std::integral_constant<int, 0>{}, kt);
+    step(std::integral_constant<int, 1>{}, kt + 1);
+    step(std::integral_constant<int, 2>{}, kt + 2);
+    if constexpr (STAGES > 3) step(std::integral_constant<int, 3>{}, kt + 3);
+  }
+  if (kt < nk) step(std::integral_constant<int, 0>{}, kt);
+  if (kt + 1 < nk) step(std::integral_constant<int, 1>{}, kt + 1);
+  if constexpr (STAGES > 3)
+    if (kt + 2 < nk) step(std::integral_constant<int, 2>{}, kt + 2);
+  // the zero-filling loads past K land before the buffers are reused
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  if constexpr (KSPLIT == 2) {
+    // the second K half's partial sums go through LDS (lane-major, so each lane reads
+    // back exactly what its partner wrote) to the first half's wavefronts: one fixed
+    // order (first half + second half) for every element
+    auto part = [&](int i, int j, int q) -> f32x4* {
+      const int b = i * TN + j;
+      const int st = b % STAGES;
+      char* base = st == 0 ? st0 : st == 1 ? st1 : st == 2 ? st2 : st3;
+      return (f32x4*)(base + (b / STAGES) * PBLK) + (wmn * 4 + q) * 64 + lane;
+    };
+    if (kg == 1) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            *part(i, j, q) = f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+    }
+    __syncthreads();
+    if (kg == 0) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = *part(i, j, q);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += v[e];
+          }
+    }
+    __syncthreads();
+  }
+  if constexpr (kBf16Out) {
+    bf16_epilogue<KIND, BM, BN, TM, TN, NT>(a, acc, (bf16*)st0, bias_s, m0, n0, wm, wn, l32, g, kg == 0, tid);
+  } else {
+    // two passes of BM / 2 rows, staged in stages 0 and 1
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      float* Cs = (float*)(p == 0 ? st0 : st1);
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int rb0 = (wm * TM + i) * 32;
+        if (kg != 0 || rb0 < p * RP || rb0 >= (p + 1) * RP) continue;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            *(f32x4*)&Cs[(rb0 - p * RP + l32) * CP + (wn * TN + j) * 32 + q * 8 + g * 4] = v;
+          }
+      }
+      __syncthreads();
+      staged_epilogue<KIND, RP, BN, NT>(a, Cs, CP, m0 + p * RP, n0, tid);
+    }
+  }
+}
+
 // ------------------------------------------------------------------ fp32 / FMA
 constexpr int kFT = 64;   // tile edge
 constexpr int kFK = 16;   // K slice
@@ -540,6 +830,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   X(2, 128, 384, 64, 2, 4, 1)     \
   X(6, 128, 128, 128, 2, 2, 2)
 
+// Directly staged tiles (as above, plus the number of LDS stages).
+#define SF_GEMM_DMA_TILES(X)           \
+  X(7, 128, 96, 64, 4, 1, 2, 4)
+
 struct TileInfo {
   int bm, bn, waves;
 };
@@ -560,6 +854,13 @@ static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
     break;
     SF_GEMM_TILES(SF_TILE_CASE)
 #undef SF_TILE_CASE
+#define SF_DMA_TILE_CASE(id, bm, bn, bk, wm, wn, ks, st)                                           \
+  case id:                                                                                         \
+    launch((gemm_bf16_dma_kernel<bm, bn, bk, wm, wn, ks, st, KIND>),                               \
+           dim3(((a.N + bn - 1) / bn) * ((a.M + bm - 1) / bm)), dim3(wm * wn * ks * 64), 0, s, a); \
+    break;
+    SF_GEMM_DMA_TILES(SF_DMA_TILE_CASE)
+#undef SF_DMA_TILE_CASE
     default:
       return hipErrorInvalidValue;
   }
@@ -568,19 +869,22 @@ static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
 
 // Tiles chosen from measurements on the 512^2 and 1024^2 projection shapes. Narrow
 // outputs (N <= 768, e.g. the attention output and MLP down-projections of the width-768
-// network) take 128x128 tiles with 128-wide K slices split over two sets of wavefronts:
-// with few output columns there are too few wide tiles to fill the chip, and the second
-// wavefront set keeps the matrix cores fed while loads are in flight. (At N = 1152 the
-// 128x128 tiles outnumber the CUs, and the split tile, one workgroup per CU, loses to
-// the plain one, two per CU: 72 vs 67 us on 4096x1152x4608.) The partial sums of the two
-// halves are added in a fixed order, and the choice depends on N and K only, never on
-// M, so a row's result does not depend on how many rows are in the batch. Otherwise
-// 128x128 (64x64 per wavefront) is the general tile; 128x384 and 128x288 (64x96 per
-// wavefront, 8 and 6 wavefronts) win when they cut the problem into exactly one
-// workgroup per CU (e.g. 4096x3072 and 4096x2304); these three accumulate in the same
-// order, so switching among them with M changes no result bit.
+// network) have too few wide tiles to fill the chip, so they take the directly staged
+// 128x96 tile (exactly one workgroup per CU at 4096x768) with each 64-wide K slice split
+// over two sets of wavefronts (4096x768x3072: 28.2 us, against 29.5 for the
+// register-staged 128x128 tile with 128-wide split slices, which remains for other
+// multiples of 128 up to 768). (At N = 1152 the 128x128 tiles outnumber the CUs, and a
+// split tile, one workgroup per CU, loses to the plain one, two per CU: 72 vs 67 us on
+// 4096x1152x4608.) The partial sums of the two halves are added in a fixed order, and
+// the choice depends on N and K only, never on M, so a row's result does not depend on
+// how many rows are in the batch. Otherwise 128x128 (64x64 per wavefront) is the
+// general tile; 128x384 and 128x288 (64x96 per wavefront, 8 and 6 wavefronts) win when
+// they cut the problem into exactly one workgroup per CU (e.g. 4096x3072 and
+// 4096x2304); these three accumulate in the same order, so switching among them with M
+// changes no result bit.
 int choose_gemm_tile(int M, int N, int K) {
   (void)K;
+  if (N % 96 == 0 && N <= 768) return 7;
   if (N % 128 == 0 && N <= 768) return 6;
   auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
   if (M % 128 == 0 && N % 384 == 0 && tiles(128, 384) == 256) return 2;
