@@ -237,6 +237,211 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   }
 }
 
+// Head dim 64: the same computation with the K and V^T tiles moved by buffer_load ... lds
+// straight from global memory into a ring of three LDS stages, two steps ahead (no VGPR
+// round trip, no LDS write instructions). Each stage is its own __shared__ variable
+// and the key loop is unrolled by three, so the compiler waits only for the stage being
+// read; the barrier is a bare s_barrier after an explicit wait for this step's loads.
+// A stage holds the step's 64 keys: K as 64 rows x 8 chunks (dh) and V^T as 64 dh rows
+// x 8 chunks (keys), both swizzled with dma_swz; 16 KB, so three workgroups of three
+// stages fit a CU.
+constexpr int kAttnStages = 3;
+
+__global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
+  constexpr int DH = 64, DHC = 4, DB = 2, CPR = 8;
+  constexpr int KCHUNKS = 2 * kKH * CPR;  // 512
+  constexpr int SB = (KCHUNKS + DH * CPR) * 16;
+  constexpr int LPT = SB / 16 / 256;  // loads per thread and step
+  constexpr int MERGE = 64 * (DB * 16 + 2) * 4;
+  static_assert(MERGE <= SB && LPT == 4, "stage layout");
+  __shared__ __attribute__((aligned(16))) char st0[SB];
+  __shared__ __attribute__((aligned(16))) char st1[SB];
+  __shared__ __attribute__((aligned(16))) char st2[SB];
+  auto stage = [&](auto s) -> char* {
+    constexpr int S = decltype(s)::value % kAttnStages;
+    if constexpr (S == 0) return st0;
+    else if constexpr (S == 1) return st1;
+    else return st2;
+  };
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int qg = wave & 1, kh = wave >> 1;
+  const int l32 = lane & 31, g = lane >> 5;
+  const int nqb = (a.Nq + kQB - 1) / kQB;
+  const int T = nqb * a.heads * a.rows;
+  const int xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  const int base = T / 8, rem = T % 8;
+  const int logical = xcd * base + min(xcd, rem) + local;
+  const int qblk = logical % nqb;
+  const int rh = logical / nqb;
+  const int head = rh % a.heads, r = rh / a.heads;
+  const size_t bh = (size_t)r * a.heads + head;
+  const bf16* Q = (const bf16*)a.q + bh * a.Nq * DH;
+  const bf16* Kg = (const bf16*)a.k + bh * a.Nk * DH;
+  const bf16* Vt = (const bf16*)a.vT + bh * DH * a.ldv;
+  const int qi = qblk * kQB + qg * 32 + l32;
+
+  bf16x8 qf[DHC];
+  const __amdgpu_buffer_rsrc_t q_src = buffer_rsrc(Q, (uint32_t)a.Nq * DH * 2);
+#pragma unroll
+  for (int kk = 0; kk < DHC; ++kk) {
+    const u32x4 w = buffer_load16(q_src, qi < a.Nq ? (qi * DH + kk * 16 + g * 8) * 2 : kOffOOB);
+    qf[kk] = __builtin_bit_cast(bf16x8, w);
+  }
+
+  // load i of a thread fills chunk position p = i * 256 + tid of a stage: K row (key)
+  // p / 8 for i < 2, else V^T row (dh) p / 8 - 64; position p % 8 holds chunk
+  // (p % 8) ^ swz(row) of that row (dh columns of K, key columns of V^T)
+  const __amdgpu_buffer_rsrc_t k_src = buffer_rsrc(Kg, (uint32_t)a.Nk * DH * 2);
+  const __amdgpu_buffer_rsrc_t v_src = buffer_rsrc(Vt, (uint32_t)DH * a.ldv * 2);
+  int goff[LPT], gkey[LPT];
+#pragma unroll
+  for (int i = 0; i < LPT; ++i) {
+    const int p = i * 256 + tid;
+    const int row = (p / CPR) % 64;
+    const int c = (p % CPR) ^ dma_swz<CPR>(row);
+    if (i < 2) {
+      gkey[i] = row;  // key of the step
+      goff[i] = (row * DH + c * 8) * 2;
+    } else {
+      gkey[i] = c * 8;  // first key of the chunk
+      goff[i] = (row * a.ldv + c * 8) * 2;
+    }
+  }
+  auto issue = [&](char* sb, int step) {
+    const int kv0 = step * 2 * kKH;
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      const int off = i < 2 ? (kv0 + gkey[i] < a.Nk ? goff[i] + kv0 * DH * 2 : kOffOOB)
+                            : (kv0 + gkey[i] < a.ldv ? goff[i] + kv0 * 2 : kOffOOB);
+      buffer_load16_lds(i < 2 ? k_src : v_src, sb + (i * 256 + wave * 64) * 16, off);
+    }
+  };
+
+  f32x16 o[DB];
+#pragma unroll
+  for (int b = 0; b < DB; ++b)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[b][e] = 0.0f;
+  float m2 = -INFINITY, lsum = 0.0f;
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const int sw = dma_swz<CPR>(l32);  // the swizzle of every row this lane reads
+  const int krow = (kh * kKH + l32) * CPR;
+
+  constexpr int kWait = waitcnt_vm_lgkm0<(kAttnStages - 2) * LPT>();
+  auto step = [&](auto s, int it) {
+    constexpr int S = decltype(s)::value;
+    __builtin_amdgcn_s_waitcnt(kWait);
+    bare_barrier();
+    issue(stage(std::integral_constant<int, S + kAttnStages - 1>{}), it + kAttnStages - 1);
+    const char* cur = stage(std::integral_constant<int, S>{});
+    const int kv0 = it * 2 * kKH + kh * kKH;
+    f32x16 sc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) sc[e] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < DHC; ++kk) {
+      const bf16x8 kf = *(const bf16x8*)(cur + (krow + ((kk * 2 + g) ^ sw)) * 16);
+      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sc, 0, 0, 0);
+    }
+    if (kv0 + kKH > a.Nk) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) sc[e] = -INFINITY;
+    }
+    float tmax = sc[0];
+#pragma unroll
+    for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[e]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+    if (__any(tmax > m2 + kLazy)) {
+      const float mnew = fmaxf(m2, tmax);
+      const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
+      lsum *= alpha;
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
+      m2 = mnew;
+    }
+    bf16x8 pf[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[ks * 8 + j], sl2, -m2));
+        lsum += p;
+        pf[ks][j] = (bf16)p;
+      }
+    }
+    // V^T fragment of k-slots 8g..8g+7: keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
+    // of this half, i.e. 8-byte half g of key chunks kh*4 + 2 ks and kh*4 + 2 ks + 1
+#pragma unroll
+    for (int b = 0; b < DB; ++b) {
+      const char* vrow = cur + KCHUNKS * 16 + (b * 32 + l32) * CPR * 16 + g * 8;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int c0 = kh * 4 + 2 * ks;
+        const bf16x4 lo = *(const bf16x4*)(vrow + ((c0 ^ sw) << 4));
+        const bf16x4 hi = *(const bf16x4*)(vrow + (((c0 + 1) ^ sw) << 4));
+        const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
+      }
+    }
+  };
+
+  const int nsteps = (a.Nk + 2 * kKH - 1) / (2 * kKH);
+  issue(stage(std::integral_constant<int, 0>{}), 0);
+  issue(stage(std::integral_constant<int, 1>{}), 1);
+  // whole rounds of three steps in a loop with one exit, then the remaining steps
+  int it = 0;
+  for (; it + kAttnStages <= nsteps; it += kAttnStages) {
+    step(std::integral_constant<int, 0>{}, it);
+    step(std::integral_constant<int, 1>{}, it + 1);
+    step(std::integral_constant<int, 2>{}, it + 2);
+  }
+  if (it < nsteps) step(std::integral_constant<int, 0>{}, it);
+  if (it + 1 < nsteps) step(std::integral_constant<int, 1>{}, it + 1);
+  // the zero-filling loads past the keys land before the stages are reused
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  // merge the key halves: half 1 hands (o, max, partial sum) to half 0 through LDS
+  float* mg = (float*)(qg == 0 ? st0 : st1);
+  if (kh == 1) {
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mg[(b * 16 + e) * 64 + lane] = o[b][e];
+    mg[DB * 16 * 64 + lane] = m2;
+    mg[(DB * 16 + 1) * 64 + lane] = lsum;
+  }
+  __syncthreads();
+  if (kh == 1) return;
+  const float m2b = mg[DB * 16 * 64 + lane];
+  const float mnew = fmaxf(m2, m2b);
+  const float a0 = m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2 - mnew);
+  const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
+  lsum = lsum * a0 + mg[(DB * 16 + 1) * 64 + lane] * a1;
+  lsum += __shfl_xor(lsum, 32);
+  const float inv = 1.0f / lsum;
+  if (qi < a.Nq) {
+    bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi) * a.D + (size_t)head * DH;
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int d = b * 32 + e4 * 8 + g * 4;
+        float w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int e = e4 * 4 + q;
+          w[q] = (o[b][e] * a0 + mg[(b * 16 + e) * 64 + lane] * a1) * inv;
+        }
+        *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
+      }
+  }
+}
+
 // ------------------------------------------------------------------ fp32
 constexpr int kFKV = 32;
 
@@ -307,7 +512,12 @@ hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
       case 1: launch_bf16_inst<1, 1>(a, s); break;
       case 2: launch_bf16_inst<2, 1>(a, s); break;
       case 3: launch_bf16_inst<3, 2>(a, s); break;
-      case 4: launch_bf16_inst<4, 2>(a, s); break;
+      case 4:
+        if (a.dh == 64)
+          launch(attn_bf16_dma64_kernel, dim3(((a.Nq + kQB - 1) / kQB) * a.heads * a.rows), dim3(256), 0, s, a);
+        else
+          launch_bf16_inst<4, 2>(a, s);
+        break;
       case 5: launch_bf16_inst<5, 3>(a, s); break;
       case 6: launch_bf16_inst<6, 3>(a, s); break;
       case 7: launch_bf16_inst<7, 4>(a, s); break;

@@ -493,43 +493,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
 // explicit wait for this slice's loads: the workgroup-scope release fence of
 // __syncthreads would wait for every outstanding LDS-bound load, i.e. for all stages.
 //
-// Stage layout: rows of BK bf16 without padding; 16-byte chunk c of row r sits at chunk
-// position c ^ swz(r), which keeps the fragment reads (one row per lane, lanes 0-15 and
-// 16-31 each reading one chunk column of 16 consecutive rows) free of bank conflicts
-// whether the LDS serves 8 or 16 lanes of a 16-byte read per cycle.
-template <int CPR>
-__device__ __forceinline__ int dma_swz(int r) {
-  static_assert(CPR == 8 || CPR == 16, "8 or 16 chunks per row");
-  if constexpr (CPR == 8)
-    return (r & 7) ^ ((r >> 3) & 1);
-  else
-    return r & 15;
-}
-
-// A non-template wrapper: with the builtin written inside the kernel template the
-// host-side pass of this compiler dropped the kernels' launch stubs.
-__device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, char* lds, int off) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
-}
-
-// Workgroup barrier without a memory fence; the signal fences keep the compiler from
-// moving LDS accesses across it. Callers wait for what the barrier must cover first.
-__device__ __forceinline__ void bare_barrier() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_barrier();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
-
-template <int N>
-__device__ __forceinline__ constexpr int waitcnt_vm_only() {
-  static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
-  return (N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8);
-}
-template <int N>
-__device__ __forceinline__ constexpr int waitcnt_vm_lgkm0() {
-  static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
-  return (N & 15) | ((N >> 4) << 14) | (7 << 4);
-}
+// Stage layout: rows of BK bf16 without padding, 16-byte chunks swizzled by dma_swz.
 
 template <int BM, int BN, int BK, int WM, int WN, int KSPLIT, int STAGES, EpiKind KIND>
 __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(GemmArgs a) {

@@ -103,4 +103,40 @@ __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, int off
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
 
+// ---- direct global -> LDS staging (buffer_load ... lds) ---------------------------
+// Unpadded LDS tiles of 8 or 16 16-byte chunks per row: chunk c of row r sits at chunk
+// position c ^ dma_swz(r), which keeps 16-byte fragment reads (one row per lane, lanes
+// 0-15 and 16-31 each reading one chunk column of 16 consecutive rows) free of bank
+// conflicts whether the LDS serves 8 or 16 lanes of a 16-byte read per cycle. The
+// swizzle depends on r % 16 only, so rows 32 apart share it.
+template <int CPR>
+__device__ __forceinline__ int dma_swz(int r) {
+  static_assert(CPR == 8 || CPR == 16, "8 or 16 chunks per row");
+  if constexpr (CPR == 8)
+    return (r & 7) ^ ((r >> 3) & 1);
+  else
+    return r & 15;
+}
+
+// A non-template wrapper: with the builtin written inside the kernel template the
+// host-side pass of this compiler dropped the kernels' launch stubs.
+__device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, char* lds, int off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
+}
+
+// Workgroup barrier without a memory fence; the signal fences keep the compiler from
+// moving LDS accesses across it. Callers wait for what the barrier must cover first.
+__device__ __forceinline__ void bare_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// s_waitcnt immediate: at most N vector-memory operations outstanding, no LDS ones.
+template <int N>
+__device__ __forceinline__ constexpr int waitcnt_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
+  return (N & 15) | ((N >> 4) << 14) | (7 << 4);
+}
+
 }  // namespace sf

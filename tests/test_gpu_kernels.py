@@ -46,7 +46,7 @@ def _run_block0(name, prec):
 
 
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
-@pytest.mark.parametrize("name", ["tiny_tsens", "ragged", "dh72"])
+@pytest.mark.parametrize("name", ["tiny_tsens", "ragged", "dh72", "dh64"])
 def test_block0_intermediates(name, prec):
     cfg, om, g, tr = _run_block0(name, prec)
     b = om.blocks[0]

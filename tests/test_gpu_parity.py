@@ -15,7 +15,7 @@ from gpu_util import dev, host, model, torch  # noqa: E402
 
 TOL = {"fp32": TOL_FP32, "bf16": TOL_BF16}
 PRECS = ["fp32", "bf16"]
-SMALL = ["tiny", "tiny_tsens", "ragged", "dh72"]
+SMALL = ["tiny", "tiny_tsens", "ragged", "dh72", "dh64"]
 
 
 def _inputs(name):
@@ -89,7 +89,7 @@ def test_modulation_table_rows_are_per_sample(prec):
 # ------------------------------------------------------------- residual per block
 
 @pytest.mark.parametrize("prec", PRECS)
-@pytest.mark.parametrize("name", ["tiny_tsens", "ragged", "dh72"])
+@pytest.mark.parametrize("name", ["tiny_tsens", "ragged", "dh72", "dh64"])
 def test_residual_stream_per_block(name, prec):
     cfg, x, t, _ = _inputs(name)
     om = oracle_model(name)
@@ -135,7 +135,7 @@ def test_stream_step_parity(name, prec):
 # -------------------------------------------------------- method invariants on GPU
 
 @pytest.mark.parametrize("prec", PRECS)
-@pytest.mark.parametrize("name", ["tiny_tsens", "ragged", "dh72"])
+@pytest.mark.parametrize("name", ["tiny_tsens", "ragged", "dh72", "dh64"])
 def test_heterogeneous_batch_equals_each_sample_alone(name, prec):
     cfg, x, t, _ = _inputs(name)
     m = model(name, prec)

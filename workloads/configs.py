@@ -87,6 +87,9 @@ CONFIGS = {
     "ragged": Config("ragged", C=4, H=20, W=28, p=2, D=192, L=2, heads=4, mlp=768, K=3, schedule="uniform3"),
     # head dim 72 (as in the width-1152 nets) at a small size
     "dh72": Config("dh72", C=4, H=16, W=24, p=2, D=144, L=2, heads=2, mlp=576),
+    # head dim 64 (as in the width-768 nets) with a ragged token count: 300 tokens are
+    # five 64-key attention steps, the last holding 44 keys
+    "dh64": Config("dh64", C=4, H=20, W=60, p=2, D=128, L=2, heads=2, mlp=512),
     # 512^2 image: 4x64x64 latent, 1024 tokens, width 768, 12 blocks, 12 heads
     "s512": _S512,
     # 512^2, width 1152, 28 blocks, 16 heads; every slot at a different step
