@@ -117,6 +117,64 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const float* 
   }
 }
 
+// The same residual epilogue with its global operands loaded ahead of time: load()
+// issues, for one pass of RP tile rows, the bias, gate-row and residual loads of a
+// thread's items (clamped in-range addresses for items outside the tile), so their
+// latency can pass under other work; apply() combines them with the C tile staged in
+// LDS, with the arithmetic of staged_epilogue, and stores.
+template <EpiKind KIND, int RP, int BN, int NT>
+struct ResItems {
+  static_assert(KIND == EPI_RES || KIND == EPI_RES_GATE || KIND == EPI_RES_GATE_MLP || KIND == EPI_GELU ||
+                    KIND == EPI_QKV,
+                "epilogue kind");
+  static constexpr bool kGate = KIND == EPI_RES_GATE || KIND == EPI_RES_GATE_MLP;
+  static constexpr int C4 = BN / 4;
+  static constexpr int TOTAL = RP * C4;
+  static constexpr int IT = (TOTAL + NT - 1) / NT;
+  float4 b[IT], h[IT], g[IT];
+
+  __device__ __forceinline__ static bool item(const GemmArgs& a, int m0, int n0, int tid, int u, int& row, int& c4,
+                                              int& m, int& n) {
+    const int c = tid + u * NT;
+    row = c / C4;
+    c4 = c - row * C4;
+    m = m0 + row;
+    n = n0 + c4 * 4;
+    return (TOTAL % NT == 0 || c < TOTAL) && m < a.M && n < a.N;
+  }
+  __device__ __forceinline__ void load(const GemmArgs& a, int m0, int n0, int tid) {
+#pragma unroll
+    for (int u = 0; u < IT; ++u) {
+      int row, c4, m, n;
+      const bool ok = item(a, m0, n0, tid, u, row, c4, m, n);
+      const int mm = ok ? m : m0, nn = ok ? n : 0;
+      b[u] = *(const float4*)(a.bias + nn);
+      h[u] = *(const float4*)(a.h + (size_t)mm * a.ldh + nn);
+      if constexpr (kGate) {
+        const int r = (int)fdiv((uint32_t)mm, a.div_ntok);
+        const int slot = r < a.n_slots ? r : r - a.n_slots;
+        g[u] = *(const float4*)(a.table + (size_t)slot * a.ldt + a.gate_off + nn);
+      }
+    }
+  }
+  __device__ __forceinline__ void apply(const GemmArgs& a, const float* Cs, int CP, int m0, int n0, int tid) const {
+#pragma unroll
+    for (int u = 0; u < IT; ++u) {
+      int row, c4, m, n;
+      const bool ok = item(a, m0, n0, tid, u, row, c4, m, n);
+      const float4 cv = *(const float4*)&Cs[(ok ? row : 0) * CP + (ok ? c4 * 4 : 0)];
+      const float v0 = cv.x + b[u].x, v1 = cv.y + b[u].y, v2 = cv.z + b[u].z, v3 = cv.w + b[u].w;
+      float4 hh = h[u];
+      if constexpr (kGate) {
+        hh.x += g[u].x * v0; hh.y += g[u].y * v1; hh.z += g[u].z * v2; hh.w += g[u].w * v3;
+      } else {
+        hh.x += v0; hh.y += v1; hh.z += v2; hh.w += v3;
+      }
+      if (ok) *(float4*)(a.h + (size_t)m * a.ldh + n) = hh;
+    }
+  }
+};
+
 // Epilogue of the bf16-output projections (GELU for the MLP up-projection, the head
 // split for QKV). Bias and activation are applied in registers, where every lane holds
 // four adjacent columns of one row; the bf16 results are staged in LDS (8-byte writes)
@@ -674,6 +732,13 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   // the zero-filling loads past K land before the buffers are reused
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  // the residual epilogues' global operands (bias, gate row, residual) for both row
+  // halves are loaded now: their latency passes under the K-split merge and the staging
+  ResItems<KIND, RP, BN, NT> pre[2];
+  if constexpr (!kBf16Out) {
+    pre[0].load(a, m0, n0, tid);
+    pre[1].load(a, m0 + RP, n0, tid);
+  }
 
   if constexpr (KSPLIT == 2) {
     // the second K half's partial sums go through LDS (lane-major, so each lane reads
@@ -712,7 +777,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   if constexpr (kBf16Out) {
     bf16_epilogue<KIND, BM, BN, TM, TN, NT>(a, acc, (bf16*)st0, bias_s, m0, n0, wm, wn, l32, g, kg == 0, tid);
   } else {
-    // two passes of BM / 2 rows, staged in stages 0 and 1
+    // the two row halves of the tile staged in stages 0 and 1 under one barrier
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
       float* Cs = (float*)(p == 0 ? st0 : st1);
@@ -728,9 +793,10 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
             *(f32x4*)&Cs[(rb0 - p * RP + l32) * CP + (wn * TN + j) * 32 + q * 8 + g * 4] = v;
           }
       }
-      __syncthreads();
-      staged_epilogue<KIND, RP, BN, NT>(a, Cs, CP, m0 + p * RP, n0, tid);
     }
+    __syncthreads();
+    pre[0].apply(a, (const float*)st0, CP, m0, n0, tid);
+    pre[1].apply(a, (const float*)st1, CP, m0 + RP, n0, tid);
   }
 }
 
@@ -792,7 +858,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   X(0, 128, 128, 64, 2, 2, 1)     \
   X(1, 128, 288, 64, 2, 3, 1)     \
   X(2, 128, 384, 64, 2, 4, 1)     \
-  X(6, 128, 128, 128, 2, 2, 2)
+  X(6, 128, 128, 128, 2, 2, 2)     \
+  X(3, 256, 192, 64, 4, 2, 1)
 
 // Directly staged tiles (as above, plus the number of LDS stages).
 #define SF_GEMM_DMA_TILES(X)           \
@@ -844,8 +911,10 @@ static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
 // how many rows are in the batch. Otherwise 128x128 (64x64 per wavefront) is the
 // general tile; 128x384 and 128x288 (64x96 per wavefront, 8 and 6 wavefronts) win when
 // they cut the problem into exactly one workgroup per CU (e.g. 4096x3072 and
-// 4096x2304); these three accumulate in the same order, so switching among them with M
-// changes no result bit.
+// 4096x2304), and 256x192 (64x96 per wavefront, 8 wavefronts) when its tiles fill whole
+// rounds of 256 workgroups (e.g. 16384x4608, the 1024^2 MLP up-projection: 184 us
+// against 192 for 128x128); these four accumulate in the same order, so switching among
+// them with M changes no result bit.
 int choose_gemm_tile(int M, int N, int K) {
   (void)K;
   if (N % 96 == 0 && N <= 768) return 7;
@@ -853,6 +922,7 @@ int choose_gemm_tile(int M, int N, int K) {
   auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
   if (M % 128 == 0 && N % 384 == 0 && tiles(128, 384) == 256) return 2;
   if (M % 128 == 0 && N % 288 == 0 && tiles(128, 288) == 256) return 1;
+  if (M % 256 == 0 && N % 192 == 0 && tiles(256, 192) % 256 == 0) return 3;
   return 0;
 }
 
