@@ -237,6 +237,20 @@ int sf_graph_enable(sf_model* m, int enable);
 /* Number of graphs currently cached and number of replays served from the cache. */
 int sf_graph_stats(const sf_model* m, int* cached, long* replays);
 
+/* Modulation cache (the per-sample conditioning computed once while the timesteps stay
+ * the same). The adaLN table of a call depends on its timesteps only (Eq. 5: each
+ * sample's own t enters the network through the timestep embedding, Sec. 3.2), and in
+ * the steady state of a fixed schedule every queue slot sees the same t at every step
+ * (Alg. 2). While enabled, sf_velocity and sf_stream_step skip the conditioning launches
+ * (timestep MLP and adaLN projections) when the previous network call on the same stream
+ * computed the table for exactly the same t[0..B) (bitwise); results are bit-identical
+ * to calls without the cache. Off by default. Enabling or disabling forgets the cached
+ * state; a failed call invalidates it. The cache assumes stream order: a call on another
+ * stream never hits it. Returns SF_E_NOTLOADED for a null model. */
+int sf_modulation_cache(sf_model* m, int enable);
+/* Number of network calls that reused the cached table (skips counted at enqueue). */
+int sf_modulation_cache_stats(const sf_model* m, long* skips);
+
 /* Test and bench hook: while enabled, every launch of kernel class `kc` is timed by a
  * pair of HIP events. For a class that is one kernel the events are attached to that
  * kernel's dispatch (its own start and end); SF_KC_TEMB and SF_KC_CROSS, which launch

@@ -90,6 +90,8 @@ _SIGS = {
     "sf_set_scheduler": (_I, [_P, ctypes.POINTER(_PeRFlow)]),
     "sf_scheduler_shift": (_I, [_P, _P, _P, _P, _P, _I, _P, _P, _P]),
     "sf_graph_stats": (_I, [_P, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_long)]),
+    "sf_modulation_cache": (_I, [_P, _I]),
+    "sf_modulation_cache_stats": (_I, [_P, ctypes.POINTER(ctypes.c_long)]),
 }
 
 
@@ -297,6 +299,16 @@ class Model:
         cached, replays = ctypes.c_int(), ctypes.c_long()
         _check(load_library().sf_graph_stats(self._h, ctypes.byref(cached), ctypes.byref(replays)), "sf_graph_stats")
         return cached.value, replays.value
+
+    def modulation_cache(self, on=True):
+        """Skip the per-sample conditioning launches when a call's timesteps equal the
+        previous network call's on the same stream (see sf_modulation_cache)."""
+        _check(load_library().sf_modulation_cache(self._h, 1 if on else 0), "sf_modulation_cache")
+
+    def modulation_cache_stats(self):
+        skips = ctypes.c_long()
+        _check(load_library().sf_modulation_cache_stats(self._h, ctypes.byref(skips)), "sf_modulation_cache_stats")
+        return skips.value
 
     def timing_enable(self, kc, on=True):
         _check(load_library().sf_timing_enable(self._h, int(kc), 1 if on else 0), "sf_timing_enable")

@@ -118,6 +118,14 @@ struct sf_model {
   std::vector<GraphEntry> graphs;
   unsigned long long graph_clock = 0;
   long graph_replays = 0;
+  // modulation cache: the timesteps (and stream) the adaLN table rows were last
+  // computed for, so a call with the same timesteps can skip the conditioning launches
+  bool mod_cache_on = false;
+  bool mod_valid = false;
+  int mod_n = 0;
+  float mod_t[SF_MAX_ROWS] = {};
+  hipStream_t mod_stream = nullptr;
+  long mod_skips = 0;
 };
 
 namespace {
@@ -386,10 +394,10 @@ sf::GemmArgs gemm_base(const void* A, int lda, const void* B, int ldb, int M, in
 // with guidance: cond rows then uncond rows, each using its latent's t). Runs through
 // `nblocks` blocks; if head_out != nullptr also the output head into head_out [rows][E].
 int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows, const sf_cond* cond,
-                int nblocks, float* head_out, hipStream_t s) {
+                int nblocks, float* head_out, hipStream_t s, bool table_ready = false) {
   const Header& h = m->hd;
   const int D = h.D, N = m->N, M = rows * N;
-  SF_TRY(run_modulation(m, t, n_lat, m->table, s));
+  if (!table_ready) SF_TRY(run_modulation(m, t, n_lat, m->table, s));
   SF_TRY(timed(m, SF_KC_EMBED, s, [&]() {
     sf::EmbedArgs e{x, n_lat, m->W_pe, m->b_pe, m->pos, m->h, rows, (int)h.C, (int)h.H, (int)h.W, (int)h.p, D, N};
     return sf::launch_embed(e, s);
@@ -504,6 +512,27 @@ void set_windows(const sf_model* m, const float* t, int B, sf::EulerArgs& a) {
   for (int i = 0; i < B; ++i) a.t.v[i] = t[i];
 }
 
+// ---------------------------------------------------------------- modulation cache
+// True when the cache is on and the adaLN table already holds the rows of exactly these
+// timesteps (bitwise), computed by an earlier call on the same stream: the call can then
+// skip the conditioning launches (the table depends on t only).
+bool modulation_cached(const sf_model* m, const float* t, int n, hipStream_t s) {
+  return m->mod_cache_on && m->mod_valid && m->mod_n == n && m->mod_stream == s &&
+         std::memcmp(m->mod_t, t, sizeof(float) * n) == 0;
+}
+
+// Records what a network call left in the table: the rows of t[0..n) if it computed them
+// (or reused them) and succeeded; nothing valid otherwise.
+int note_modulation(sf_model* m, const float* t, int n, hipStream_t s, int rc) {
+  m->mod_valid = rc == SF_OK;
+  if (m->mod_valid) {
+    m->mod_n = n;
+    std::memcpy(m->mod_t, t, sizeof(float) * n);
+    m->mod_stream = s;
+  }
+  return rc;
+}
+
 // ---------------------------------------------------------------- graph replay
 constexpr size_t kMaxGraphs = 64;
 
@@ -514,9 +543,11 @@ void key_put(std::vector<char>& k, const T& v) {
 }
 
 std::vector<char> call_key(int kind, const void* a, const void* b, const void* c, const void* d, int B,
-                           const float* t, const float* dt, const sf_cond* cond, hipStream_t s) {
+                           const float* t, const float* dt, const sf_cond* cond, hipStream_t s,
+                           bool table_ready) {
   std::vector<char> k;
   key_put(k, kind);
+  key_put(k, table_ready);
   key_put(k, a);
   key_put(k, b);
   key_put(k, c);
@@ -709,11 +740,14 @@ int sf_velocity(sf_model* m, const float* x, const float* t, int B, const sf_con
   const int rows = rows_for(m, B, cond, &guided, &w);
   if (!rows) return SF_E_INVAL;
   hipStream_t s = (hipStream_t)stream;
-  return run_graphed(m, call_key(0, x, v, nullptr, nullptr, B, t, nullptr, cond, s), s, [&]() -> int {
-    SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, guided ? m->vrows : v, s));
+  const bool ready = modulation_cached(m, t, B, s);
+  if (ready) ++m->mod_skips;
+  const int rc = run_graphed(m, call_key(0, x, v, nullptr, nullptr, B, t, nullptr, cond, s, ready), s, [&]() -> int {
+    SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, guided ? m->vrows : v, s, ready));
     if (guided) return timed(m, SF_KC_EULER, s, [&]() { return sf::launch_cfg_combine(m->vrows, B, m->E, w, v, s); });
     return SF_OK;
   });
+  return note_modulation(m, t, B, s, rc);
 }
 
 int sf_stream_step(sf_model* m, float* x, const float* t, const float* dt, int B, const sf_cond* cond,
@@ -726,8 +760,10 @@ int sf_stream_step(sf_model* m, float* x, const float* t, const float* dt, int B
   const int rows = rows_for(m, B, cond, &guided, &w);
   if (!rows) return SF_E_INVAL;
   hipStream_t s = (hipStream_t)stream;
-  return run_graphed(m, call_key(1, x, z_new, x_done, nullptr, B, t, dt, cond, s), s, [&]() -> int {
-    SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, m->vrows, s));
+  const bool ready = modulation_cached(m, t, B, s);
+  if (ready) ++m->mod_skips;
+  const int rc = run_graphed(m, call_key(1, x, z_new, x_done, nullptr, B, t, dt, cond, s, ready), s, [&]() -> int {
+    SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, m->vrows, s, ready));
     return timed(m, SF_KC_EULER, s, [&]() {
       sf::EulerArgs a{};
       a.x = x; a.v = m->vrows; a.B = B; a.E = m->E; a.guided = guided ? 1 : 0; a.w = w;
@@ -737,6 +773,7 @@ int sf_stream_step(sf_model* m, float* x, const float* t, const float* dt, int B
       return sf::launch_euler_shift(a, s);
     });
   });
+  return note_modulation(m, t, B, s, rc);
 }
 
 int sf_euler_shift(sf_model* m, float* x, const float* v, const float* dt, int B, const float* z_new,
@@ -770,7 +807,7 @@ int sf_residual(sf_model* m, const float* x, const float* t, int B, const sf_con
   const int rows = rows_for(m, B, cond, &guided, &w);
   if (!rows) return SF_E_INVAL;
   hipStream_t s = (hipStream_t)stream;
-  SF_TRY(run_network(m, x, t, B, rows, cond, blocks, nullptr, s));
+  SF_TRY(note_modulation(m, t, B, s, run_network(m, x, t, B, rows, cond, blocks, nullptr, s)));
   if (hipMemcpyAsync(hout, m->h, sizeof(float) * (size_t)rows * m->N * m->hd.D, hipMemcpyDeviceToDevice, s) !=
       hipSuccess)
     return SF_E_HIP;
@@ -840,6 +877,20 @@ int sf_graph_enable(sf_model* m, int enable) {
     drop_graphs(m);
   }
   m->graph_on = enable != 0;
+  return SF_OK;
+}
+
+int sf_modulation_cache(sf_model* m, int enable) {
+  if (!m) return SF_E_NOTLOADED;
+  m->mod_cache_on = enable != 0;
+  m->mod_valid = false;
+  return SF_OK;
+}
+
+int sf_modulation_cache_stats(const sf_model* m, long* skips) {
+  if (!m) return SF_E_NOTLOADED;
+  if (!skips) return SF_E_INVAL;
+  *skips = m->mod_skips;
   return SF_OK;
 }
 

@@ -73,6 +73,8 @@ def test_calls_reject_null_handle_and_arguments():
     dummy = ctypes.c_void_p(16)
     assert L.sf_velocity(None, dummy, t, 4, None, dummy, None) == -3
     assert L.sf_graph_enable(None, 1) == -3
+    assert L.sf_modulation_cache(None, 1) == -3
+    assert L.sf_modulation_cache_stats(None, None) == -3
     assert L.sf_set_scheduler(None, None) == -3
     assert L.sf_noise_latent(None, dummy, dummy, 0.5, dummy, None) == -3
     assert L.sf_stream_step(None, dummy, t, t, 4, None, dummy, None, None) == -3
