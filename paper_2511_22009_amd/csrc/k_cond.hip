@@ -52,7 +52,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
         const int ch = lane + 64 * c;
-        w[rr][c] = buffer_load16(w_src, ch < nchunk ? (int)(((uint32_t)j * a.K + ch * E) * sizeof(WT)) : kOffOOB);
+        w[rr][c] = buffer_load16_stream(w_src, ch < nchunk ? (int)(((uint32_t)j * a.K + ch * E) * sizeof(WT)) : kOffOOB);
       }
     }
     float x[kGemvSamples][NC][E];

@@ -102,6 +102,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
 __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
+// The same load marked non-temporal (nt): for data read once per call, such as the
+// adaLN projection weights, so that streaming them does not push the projection GEMMs'
+// weights and activations out of the caches.
+__device__ __forceinline__ u32x4 buffer_load16_stream(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
+}
 
 // ---- direct global -> LDS staging (buffer_load ... lds) ---------------------------
 // Unpadded LDS tiles of 8 or 16 16-byte chunks per row: chunk c of row r sits at chunk
@@ -123,6 +129,7 @@ __device__ __forceinline__ int dma_swz(int r) {
 __device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, char* lds, int off) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
 }
+
 
 // Workgroup barrier without a memory fence; the signal fences keep the compiler from
 // moving LDS accesses across it. Callers wait for what the barrier must cover first.
