@@ -66,7 +66,8 @@ class _Info(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in
                 ("C", "H", "W", "p", "D", "L", "heads", "mlp", "tdim", "ctx_len", "ctx_dim", "has_cross",
                  "tokens", "mod_width", "precision", "max_rows")] + \
-               [("weight_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t)]
+               [("weight_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
+                ("vt_ld", ctypes.c_int), ("vt_key_perm", ctypes.c_int)]
 
 
 _LIB = None

@@ -244,7 +244,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 // read; the barrier is a bare s_barrier after an explicit wait for this step's loads.
 // A stage holds the step's 64 keys: K as 64 rows x 8 chunks (dh) and V^T as 64 dh rows
 // x 8 chunks (keys), both swizzled with dma_swz; 16 KB, so three workgroups of three
-// stages fit a CU.
+// stages fit a CU. V^T comes in the permuted key layout (vt_pos, written so by the QKV
+// projection), so each P.V fragment is one 16-byte LDS read instead of two 8-byte ones.
 constexpr int kAttnStages = 3;
 
 __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
@@ -374,16 +375,14 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
       }
     }
     // V^T fragment of k-slots 8g..8g+7: keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
-    // of this half, i.e. 8-byte half g of key chunks kh*4 + 2 ks and kh*4 + 2 ks + 1
+    // of this half, which the permuted layout (vt_pos) keeps in one 16-byte chunk,
+    // kh*4 + 2 ks + g
 #pragma unroll
     for (int b = 0; b < DB; ++b) {
-      const char* vrow = cur + KCHUNKS * 16 + (b * 32 + l32) * CPR * 16 + g * 8;
+      const char* vrow = cur + KCHUNKS * 16 + (b * 32 + l32) * CPR * 16;
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const int c0 = kh * 4 + 2 * ks;
-        const bf16x4 lo = *(const bf16x4*)(vrow + ((c0 ^ sw) << 4));
-        const bf16x4 hi = *(const bf16x4*)(vrow + (((c0 + 1) ^ sw) << 4));
-        const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const bf16x8 vf = *(const bf16x8*)(vrow + (((kh * 4 + 2 * ks + g) ^ sw) << 4));
         o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
       }
     }
@@ -506,6 +505,9 @@ static void launch_bf16_inst(const AttnArgs& a, hipStream_t s) {
 
 hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
   if (!attention_supports(a.dh)) return hipErrorInvalidValue;
+  // the permuted transposed-v layout is read by the head-dim-64 bf16 kernel only, and
+  // that kernel reads no other layout
+  if ((a.vperm != 0) != (use_bf16 && a.dh == 64) || (a.vperm && a.ldv % 16 != 0)) return hipErrorInvalidValue;
   if (use_bf16) {
     const int dhc = (a.dh + 15) / 16;
     switch (dhc) {

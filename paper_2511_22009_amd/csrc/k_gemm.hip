@@ -38,7 +38,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int m, int n, float 
     // the divergent if / else-if / else form to code that stored the v part through
     // the k pointer.
     const size_t i_qk = (bh * a.ntok + tok) * a.dh + d;
-    const size_t i_v = (bh * a.dh + d) * a.ldv + tok;
+    const size_t i_v = (bh * a.dh + d) * a.ldv + (a.vperm ? vt_pos(tok) : tok);
     OT* const p_qk = (OT*)(which == 0 ? a.q : a.k);
     OT* const dst = which >= 2 ? (OT*)a.vT + i_v : p_qk + i_qk;
     *dst = from_f32<OT>(val);
@@ -249,40 +249,63 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
     }
   }
   if constexpr (KIND == EPI_QKV) {
-    // transposed v: item = (column, 8 consecutive rows); skipped unless the tile
-    // reaches the v columns
+    // transposed v, skipped unless the tile reaches the v columns. Item = (column, RG
+    // consecutive rows): 8 rows, one 16-byte store, in the plain layout; 16 rows, two
+    // 16-byte stores of the permuted key order, in the vt_pos layout (a whole group of
+    // 16 keys). Items that end a network row early or start unaligned go element-wise.
     if (a.which_base + (int)fdiv((uint32_t)min(n0 + BN, a.N) - 1, a.div_D) < 2) return;
-    constexpr int R8 = BM / 8;
-    constexpr int VT = R8 * BN;
-    constexpr int VIT = (VT + NT - 1) / NT;
-    for (int it = 0; it < VIT; ++it) {
-      const int c = tid + it * NT;
-      const int r8 = c / BN, col = c - r8 * BN;  // adjacent lanes: adjacent columns
-      const int n = n0 + col, m = m0 + r8 * 8;
-      if ((VT % NT != 0 && c >= VT) || n >= a.N || m >= a.M) continue;
-      const int part = (int)fdiv((uint32_t)n, a.div_D);
-      if (a.which_base + part < 2) continue;
-      const int rem = n - part * a.D;
-      const int head = (int)fdiv((uint32_t)rem, a.div_dh);
-      const int d = rem - head * a.dh;
-      const int r = (int)fdiv((uint32_t)m, a.div_ntok);
-      const int tok = m - r * a.ntok;
-      const bf16* cp = Cs + (r8 * 8) * CPB + col;
-      bf16* vt = (bf16*)a.vT + (((size_t)r * a.heads + head) * a.dh + d) * a.ldv;
-      if (tok + 8 <= a.ntok && m + 8 <= a.M && (tok & 7) == 0) {
-        bf16x8 o;
+    auto v_items = [&](auto rg) {
+      constexpr int RG = decltype(rg)::value;
+      constexpr int VT = BM / RG * BN;
+      constexpr int VIT = (VT + NT - 1) / NT;
+      for (int it = 0; it < VIT; ++it) {
+        const int c = tid + it * NT;
+        const int rb = c / BN, col = c - rb * BN;  // adjacent lanes: adjacent columns
+        const int n = n0 + col, m = m0 + rb * RG;
+        if ((VT % NT != 0 && c >= VT) || n >= a.N || m >= a.M) continue;
+        const int part = (int)fdiv((uint32_t)n, a.div_D);
+        if (a.which_base + part < 2) continue;
+        const int rem = n - part * a.D;
+        const int head = (int)fdiv((uint32_t)rem, a.div_dh);
+        const int d = rem - head * a.dh;
+        const int r = (int)fdiv((uint32_t)m, a.div_ntok);
+        const int tok = m - r * a.ntok;
+        const bf16* cp = Cs + (rb * RG) * CPB + col;
+        bf16* vt = (bf16*)a.vT + (((size_t)r * a.heads + head) * a.dh + d) * a.ldv;
+        if (tok + RG <= a.ntok && m + RG <= a.M && (tok & (RG - 1)) == 0) {
+          if constexpr (RG == 8) {
+            bf16x8 o;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = cp[e * CPB];
-        *(bf16x8*)(vt + tok) = o;
-      } else {
-        for (int e = 0; e < 8 && m + e < a.M; ++e) {
-          const int me = m + e;
-          const int re = (int)fdiv((uint32_t)me, a.div_ntok);
-          const int te = me - re * a.ntok;
-          ((bf16*)a.vT)[(((size_t)re * a.heads + head) * a.dh + d) * a.ldv + te] = cp[e * CPB];
+            for (int e = 0; e < 8; ++e) o[e] = cp[e * CPB];
+            *(bf16x8*)(vt + tok) = o;
+          } else {
+            // columns tok .. tok+7 hold keys +0..3, +8..11; tok+8 .. tok+15 keys +4..7, +12..15
+            bf16x8 lo, hi;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              lo[e] = cp[e * CPB];
+              lo[4 + e] = cp[(8 + e) * CPB];
+              hi[e] = cp[(4 + e) * CPB];
+              hi[4 + e] = cp[(12 + e) * CPB];
+            }
+            *(bf16x8*)(vt + tok) = lo;
+            *(bf16x8*)(vt + tok + 8) = hi;
+          }
+        } else {
+          for (int e = 0; e < RG && m + e < a.M; ++e) {
+            const int me = m + e;
+            const int re = (int)fdiv((uint32_t)me, a.div_ntok);
+            const int te = me - re * a.ntok;
+            ((bf16*)a.vT)[(((size_t)re * a.heads + head) * a.dh + d) * a.ldv + (a.vperm ? vt_pos(te) : te)] =
+                cp[e * CPB];
+          }
         }
       }
-    }
+    };
+    if (a.vperm)
+      v_items(std::integral_constant<int, 16>{});
+    else
+      v_items(std::integral_constant<int, 8>{});
   }
 }
 

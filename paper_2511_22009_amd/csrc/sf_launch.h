@@ -123,8 +123,8 @@ struct GemmArgs {
   // head (n % D) / dh, dim (n % D) % dh; row m is token m % ntok of network row m / ntok.
   void* q;
   void* k;
-  void* vT;             // [rows][heads][dh][ldv]
-  int heads, dh, D, ntok, ldv, which_base;
+  void* vT;             // [rows][heads][dh][ldv]; token t at column t, or at vt_pos(t) if vperm
+  int heads, dh, D, ntok, ldv, which_base, vperm;
   FastDiv div_ntok, div_D, div_dh;
   // EPI_RES_GATE / EPI_RES
   float* h;
@@ -141,13 +141,22 @@ hipError_t launch_gemm_tile(bool use_bf16, int tile, EpiKind kind, const GemmArg
 int choose_gemm_tile(int M, int N, int K);
 
 // ---- K4: softmax attention per (network row, head) ---------------------------------
+// Column of key t in the permuted transposed-v layout: bits 2 and 3 of t swapped, so in
+// every group of 16 keys the columns hold keys 0-3, 8-11, 4-7, 12-15. Eight adjacent
+// columns then hold the eight keys one lane half feeds into a 16-key step of the P.V
+// product (keys 4g..4g+3 and 8+4g..8+4g+3 for lane half g), read as one 16-byte
+// fragment. An involution; needs ldv to be a multiple of 16.
+__host__ __device__ constexpr int vt_pos(int t) { return (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1); }
+
 struct AttnArgs {
   const void* q;        // [rows][heads][Nq][dh]
   const void* k;        // [rows][heads][Nk][dh]
-  const void* vT;       // [rows][heads][dh][ldv], columns >= Nk are zero
+  const void* vT;       // [rows][heads][dh][ldv], columns of no key are zero; key t at
+                        // column t, or at vt_pos(t) if vperm (bf16, head dim 64 only)
   void* o;              // [rows][Nq][D], head j at columns j*dh ..
   int rows, heads, Nq, Nk, dh, ldv, D;
   float scale;          // 1 / sqrt(dh)
+  int vperm;
 };
 hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s);
 bool attention_supports(int dh);

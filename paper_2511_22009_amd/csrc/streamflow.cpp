@@ -102,6 +102,7 @@ struct sf_model {
   void *act = nullptr, *q = nullptr, *k = nullptr, *vT = nullptr, *o = nullptr, *f = nullptr;
   void *ctxA = nullptr, *kx = nullptr, *vTx = nullptr;
   int ldv = 0, ldvx = 0;
+  int vperm = 0;  // transposed v in the permuted key layout (vt_pos): bf16, head dim 64
   Timing timing[SF_KC_COUNT];
   // graph replay: captured launch sequences keyed by the call's arguments
   struct GraphEntry {
@@ -421,13 +422,13 @@ int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows
     SF_TRY(timed(m, SF_KC_QKV, s, [&]() {
       sf::GemmArgs g = gemm_base(m->act, D, b.W_qkv, D, M, 3 * D, D, b.b_qkv);
       g.q = m->q; g.k = m->k; g.vT = m->vT;
-      g.heads = h.heads; g.dh = m->dh; g.D = D; g.ntok = N; g.ldv = m->ldv; g.which_base = 0;
+      g.heads = h.heads; g.dh = m->dh; g.D = D; g.ntok = N; g.ldv = m->ldv; g.which_base = 0; g.vperm = m->vperm;
       g.div_ntok = div_n; g.div_D = div_d; g.div_dh = div_dh;
       return sf::launch_gemm(m->bf16, sf::EPI_QKV, g, s);
     }));
     SF_TRY(timed(m, SF_KC_ATTN, s, [&]() {
       sf::AttnArgs a{m->q, m->k, m->vT, m->o, rows, (int)h.heads, N, N, m->dh, m->ldv, D,
-                     (float)(1.0 / std::sqrt((double)m->dh))};
+                     (float)(1.0 / std::sqrt((double)m->dh)), m->vperm};
       return sf::launch_attention(m->bf16, a, s);
     }));
     SF_TRY(timed(m, SF_KC_PROJ, s, [&]() {
@@ -441,15 +442,16 @@ int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows
         hipError_t e = ln(0, 0, false);
         if (e != hipSuccess) return e;
         sf::GemmArgs gq = gemm_base(m->act, D, b.W_qx, D, M, D, D, b.b_qx);
-        gq.q = m->q; gq.heads = h.heads; gq.dh = m->dh; gq.D = D; gq.ntok = N; gq.which_base = 0;
+        gq.q = m->q; gq.heads = h.heads; gq.dh = m->dh; gq.D = D; gq.ntok = N; gq.which_base = 0; gq.vperm = m->vperm;
         gq.div_ntok = div_n; gq.div_D = div_d; gq.div_dh = div_dh;
         if ((e = sf::launch_gemm(m->bf16, sf::EPI_QKV, gq, s)) != hipSuccess) return e;
         sf::GemmArgs gk = gemm_base(m->ctxA, h.ctx_dim, b.W_kvx, h.ctx_dim, rows * h.ctx_len, 2 * D, h.ctx_dim, b.b_kvx);
         gk.k = m->kx; gk.vT = m->vTx; gk.heads = h.heads; gk.dh = m->dh; gk.D = D; gk.ntok = h.ctx_len;
-        gk.ldv = m->ldvx; gk.which_base = 1; gk.div_ntok = div_ctx; gk.div_D = div_d; gk.div_dh = div_dh;
+        gk.ldv = m->ldvx; gk.which_base = 1; gk.vperm = m->vperm;
+        gk.div_ntok = div_ctx; gk.div_D = div_d; gk.div_dh = div_dh;
         if ((e = sf::launch_gemm(m->bf16, sf::EPI_QKV, gk, s)) != hipSuccess) return e;
         sf::AttnArgs a{m->q, m->kx, m->vTx, m->o, rows, (int)h.heads, N, (int)h.ctx_len, m->dh, m->ldvx, D,
-                       (float)(1.0 / std::sqrt((double)m->dh))};
+                       (float)(1.0 / std::sqrt((double)m->dh)), m->vperm};
         if ((e = sf::launch_attention(m->bf16, a, s)) != hipSuccess) return e;
         sf::GemmArgs go = gemm_base(m->o, D, b.W_ox, D, M, D, D, b.b_ox);
         go.h = m->h; go.ldh = D;
@@ -659,8 +661,11 @@ int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows
   m->bf16 = precision == SF_PREC_BF16;
   m->es = m->bf16 ? 2 : 4;
   m->max_rows = max_rows;
-  m->ldv = (m->N + 7) / 8 * 8;
-  m->ldvx = h.has_cross ? (int)((h.ctx_len + 7) / 8 * 8) : 0;
+  // transposed v: rows padded to whole 16-key groups (the permuted layout moves keys
+  // within a group of 16; columns of no key stay zero from the workspace clear)
+  m->ldv = (m->N + 15) / 16 * 16;
+  m->ldvx = h.has_cross ? (int)((h.ctx_len + 15) / 16 * 16) : 0;
+  m->vperm = m->bf16 && m->dh == 64 ? 1 : 0;
 
   Carver cw;
   carve_weights(m, cw);
@@ -729,6 +734,8 @@ int sf_get_info(const sf_model* m, sf_info* info) {
   info->ctx_dim = h.ctx_dim; info->has_cross = h.has_cross; info->tokens = m->N; info->mod_width = m->modw;
   info->precision = m->prec; info->max_rows = m->max_rows; info->weight_bytes = m->wbytes;
   info->workspace_bytes = m->wsbytes;
+  info->vt_ld = m->ldv;
+  info->vt_key_perm = m->vperm;
   return SF_OK;
 }
 

@@ -26,11 +26,16 @@ def _run_block0(name, prec):
     m = model(name, prec)
     R, N, D, H, dh = cfg.K, cfg.N, cfg.D, cfg.heads, cfg.dh
     h1 = host(m.residual(dev(x), t, 1))
-    ldv = (N + 7) // 8 * 8
+    ldv = m.info["vt_ld"]
+    assert ldv % 16 == 0 and ldv >= N
+    # column of each key: the head-dim-64 bf16 layout swaps bits 2 and 3 of the key index
+    tok = np.arange(N)
+    col = (tok & ~12) | ((tok & 4) << 1) | ((tok & 8) >> 1) if m.info["vt_key_perm"] else tok
+    assert m.info["vt_key_perm"] == (prec == "bf16" and dh == 64)
     bufs = dict(
         q=host(m.debug_read(Buffer.Q, (R, H, N, dh))).transpose(0, 2, 1, 3).reshape(R, N, D),
         k=host(m.debug_read(Buffer.K, (R, H, N, dh))).transpose(0, 2, 1, 3).reshape(R, N, D),
-        v=host(m.debug_read(Buffer.VT, (R, H, dh, ldv)))[..., :N].transpose(0, 3, 1, 2).reshape(R, N, D),
+        v=host(m.debug_read(Buffer.VT, (R, H, dh, ldv)))[..., col].transpose(0, 3, 1, 2).reshape(R, N, D),
         attn=host(m.debug_read(Buffer.ATTN, (R, N, D))),
         ln2=host(m.debug_read(Buffer.ACT, (R, N, D))),
         mlp=host(m.debug_read(Buffer.MLP, (R, N, cfg.mlp))),
