@@ -80,8 +80,8 @@ typedef struct sf_info {
   size_t weight_bytes;   /* device bytes held for weights */
   size_t workspace_bytes;/* device bytes held for activations */
   int vt_ld;             /* row length (keys) of the transposed-v buffer SF_BUF_VT, a multiple of 16 */
-  int vt_key_perm;       /* 1: key t of SF_BUF_VT sits at column (t with bits 2 and 3 swapped),
-                            the layout the head-dim-64 bf16 attention reads; 0: at column t */
+  int vt_key_perm;       /* 1 (bf16 mode): key t of SF_BUF_VT sits at column (t with bits 2
+                            and 3 swapped), the layout the bf16 attention reads; 0: column t */
 } sf_info;
 
 /* Parse a weight blob, upload the weights (converted to bf16 in SF_PREC_BF16 mode) and

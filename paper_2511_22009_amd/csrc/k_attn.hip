@@ -16,7 +16,8 @@
 //     are then at most 256, which bf16 and the fp32 sums carry exactly as well;
 //   * the probabilities are rounded to bf16 and used directly as the B operand of
 //     O^T = V^T P^T: the MFMA's k-slot order is a permutation of the key order, and V^T
-//     is read from LDS under the same permutation (two 8-byte reads per fragment);
+//     is stored in that permuted key order (vt_pos, written so by the QKV projection),
+//     so a fragment is one 16-byte LDS read;
 //   * K and V^T tiles are double-buffered in LDS and fetched one step ahead through
 //     registers with raw buffer loads (keys past the end read as zeros, no branches);
 //     rows past dh and keys past Nk are zero, so padding adds nothing.
@@ -185,14 +186,13 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         pf[ks][j] = (bf16)p;
       }
     }
+    // V^T fragment of k-slots 8g..8g+7 (keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
+    // of this half): one 16-byte read in the permuted key layout (vt_pos)
 #pragma unroll
     for (int b = 0; b < DB; ++b) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const bf16* vr = &Vb[(b * 32 + l32) * VLD + ks * 16 + g * 4];
-        const bf16x4 lo = *(const bf16x4*)vr;
-        const bf16x4 hi = *(const bf16x4*)(vr + 8);
-        const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const bf16x8 vf = *(const bf16x8*)&Vb[(b * 32 + l32) * VLD + ks * 16 + g * 8];
         o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
       }
     }
@@ -505,9 +505,9 @@ static void launch_bf16_inst(const AttnArgs& a, hipStream_t s) {
 
 hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
   if (!attention_supports(a.dh)) return hipErrorInvalidValue;
-  // the permuted transposed-v layout is read by the head-dim-64 bf16 kernel only, and
-  // that kernel reads no other layout
-  if ((a.vperm != 0) != (use_bf16 && a.dh == 64) || (a.vperm && a.ldv % 16 != 0)) return hipErrorInvalidValue;
+  // the bf16 kernels read transposed v in the permuted key layout only, the fp32 kernel
+  // in the plain one
+  if ((a.vperm != 0) != use_bf16 || (a.vperm && a.ldv % 16 != 0)) return hipErrorInvalidValue;
   if (use_bf16) {
     const int dhc = (a.dh + 15) / 16;
     switch (dhc) {

@@ -152,7 +152,7 @@ struct AttnArgs {
   const void* q;        // [rows][heads][Nq][dh]
   const void* k;        // [rows][heads][Nk][dh]
   const void* vT;       // [rows][heads][dh][ldv], columns of no key are zero; key t at
-                        // column t, or at vt_pos(t) if vperm (bf16, head dim 64 only)
+                        // column t, or at vt_pos(t) if vperm (the bf16 kernels)
   void* o;              // [rows][Nq][D], head j at columns j*dh ..
   int rows, heads, Nq, Nk, dh, ldv, D;
   float scale;          // 1 / sqrt(dh)

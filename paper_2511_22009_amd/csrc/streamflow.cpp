@@ -102,7 +102,7 @@ struct sf_model {
   void *act = nullptr, *q = nullptr, *k = nullptr, *vT = nullptr, *o = nullptr, *f = nullptr;
   void *ctxA = nullptr, *kx = nullptr, *vTx = nullptr;
   int ldv = 0, ldvx = 0;
-  int vperm = 0;  // transposed v in the permuted key layout (vt_pos): bf16, head dim 64
+  int vperm = 0;  // transposed v in the permuted key layout (vt_pos): bf16 mode
   Timing timing[SF_KC_COUNT];
   // graph replay: captured launch sequences keyed by the call's arguments
   struct GraphEntry {
@@ -665,7 +665,7 @@ int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows
   // within a group of 16; columns of no key stay zero from the workspace clear)
   m->ldv = (m->N + 15) / 16 * 16;
   m->ldvx = h.has_cross ? (int)((h.ctx_len + 15) / 16 * 16) : 0;
-  m->vperm = m->bf16 && m->dh == 64 ? 1 : 0;
+  m->vperm = m->bf16 ? 1 : 0;
 
   Carver cw;
   carve_weights(m, cw);
