@@ -79,7 +79,7 @@ typedef struct sf_info {
   int max_rows;
   size_t weight_bytes;   /* device bytes held for weights */
   size_t workspace_bytes;/* device bytes held for activations */
-  int vt_ld;             /* row length (keys) of the transposed-v buffer SF_BUF_VT, a multiple of 16 */
+  int vt_ld;             /* row length (keys) of the transposed-v buffer SF_BUF_VT, a multiple of 64 */
   int vt_key_perm;       /* 1 (bf16 mode): key t of SF_BUF_VT sits at column (t with bits 2
                             and 3 swapped), the layout the bf16 attention reads; 0: column t */
 } sf_info;
@@ -158,7 +158,7 @@ int sf_residual(sf_model* m, const float* x, const float* t, int B, const sf_con
  *   SF_BUF_ACT   [rows][N][D]           last LayerNorm + modulate output (the MLP input)
  *   SF_BUF_Q/K   [rows][heads][N][dh]   self-attention queries / keys
  *   SF_BUF_VT    [rows][heads][dh][ldv] self-attention values, transposed; ldv = N
- *                                       rounded up to a multiple of 16 (sf_info.vt_ld),
+ *                                       rounded up to a multiple of 64 (sf_info.vt_ld),
  *                                       keys permuted when sf_info.vt_key_perm is 1
  *   SF_BUF_ATTN  [rows][N][D]           attention output before the output projection
  *   SF_BUF_MLP   [rows][N][mlp]         GELU(fc1) output

@@ -265,7 +265,9 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
     else return st2;
   };
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wavefront index is uniform: kept in a scalar register, so the key offsets and
+  // step checks derived from it are scalar work
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qg = wave & 1, kh = wave >> 1;
   const int l32 = lane & 31, g = lane >> 5;
   const int nqb = (a.Nq + kQB - 1) / kQB;
@@ -292,31 +294,27 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
 
   // load i of a thread fills chunk position p = i * 256 + tid of a stage: K row (key)
   // p / 8 for i < 2, else V^T row (dh) p / 8 - 64; position p % 8 holds chunk
-  // (p % 8) ^ swz(row) of that row (dh columns of K, key columns of V^T)
-  const __amdgpu_buffer_rsrc_t k_src = buffer_rsrc(Kg, (uint32_t)a.Nk * DH * 2);
-  const __amdgpu_buffer_rsrc_t v_src = buffer_rsrc(Vt, (uint32_t)DH * a.ldv * 2);
-  int goff[LPT], gkey[LPT];
+  // (p % 8) ^ swz(row) of that row (dh columns of K, key columns of V^T). Each step's
+  // loads go through buffer resources based at the step's first key, so a thread's
+  // offsets are fixed: keys past Nk fall outside the K resource and read zeros, and the
+  // V^T rows (ldv a multiple of 64) hold every key column a step can reach, zero past
+  // the last key.
+  int goff[LPT];
 #pragma unroll
   for (int i = 0; i < LPT; ++i) {
     const int p = i * 256 + tid;
     const int row = (p / CPR) % 64;
     const int c = (p % CPR) ^ dma_swz<CPR>(row);
-    if (i < 2) {
-      gkey[i] = row;  // key of the step
-      goff[i] = (row * DH + c * 8) * 2;
-    } else {
-      gkey[i] = c * 8;  // first key of the chunk
-      goff[i] = (row * a.ldv + c * 8) * 2;
-    }
+    goff[i] = i < 2 ? (row * DH + c * 8) * 2 : (row * a.ldv + c * 8) * 2;
   }
   auto issue = [&](char* sb, int step) {
     const int kv0 = step * 2 * kKH;
+    const __amdgpu_buffer_rsrc_t k_src =
+        buffer_rsrc(Kg + (size_t)kv0 * DH, (uint32_t)max(a.Nk - kv0, 0) * DH * 2);
+    const __amdgpu_buffer_rsrc_t v_src = buffer_rsrc(Vt + kv0, (uint32_t)max(DH * a.ldv - kv0, 0) * 2);
 #pragma unroll
-    for (int i = 0; i < LPT; ++i) {
-      const int off = i < 2 ? (kv0 + gkey[i] < a.Nk ? goff[i] + kv0 * DH * 2 : kOffOOB)
-                            : (kv0 + gkey[i] < a.ldv ? goff[i] + kv0 * 2 : kOffOOB);
-      buffer_load16_lds(i < 2 ? k_src : v_src, sb + (i * 256 + wave * 64) * 16, off);
-    }
+    for (int i = 0; i < LPT; ++i)
+      buffer_load16_lds(i < 2 ? k_src : v_src, sb + (i * 256 + wave * 64) * 16, goff[i]);
   };
 
   f32x16 o[DB];
@@ -515,7 +513,7 @@ hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
       case 2: launch_bf16_inst<2, 1>(a, s); break;
       case 3: launch_bf16_inst<3, 2>(a, s); break;
       case 4:
-        if (a.dh == 64)
+        if (a.dh == 64 && a.ldv % 64 == 0)
           launch(attn_bf16_dma64_kernel, dim3(((a.Nq + kQB - 1) / kQB) * a.heads * a.rows), dim3(256), 0, s, a);
         else
           launch_bf16_inst<4, 2>(a, s);

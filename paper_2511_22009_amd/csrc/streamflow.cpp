@@ -661,10 +661,12 @@ int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows
   m->bf16 = precision == SF_PREC_BF16;
   m->es = m->bf16 ? 2 : 4;
   m->max_rows = max_rows;
-  // transposed v: rows padded to whole 16-key groups (the permuted layout moves keys
-  // within a group of 16; columns of no key stay zero from the workspace clear)
-  m->ldv = (m->N + 15) / 16 * 16;
-  m->ldvx = h.has_cross ? (int)((h.ctx_len + 15) / 16 * 16) : 0;
+  // transposed v: rows padded to whole 64-key steps of the attention kernels (the
+  // permuted layout moves keys within a group of 16, and the head-dim-64 kernel loads
+  // whole steps without a column check); columns of no key stay zero from the
+  // workspace clear
+  m->ldv = (m->N + 63) / 64 * 64;
+  m->ldvx = h.has_cross ? (int)((h.ctx_len + 63) / 64 * 64) : 0;
   m->vperm = m->bf16 ? 1 : 0;
 
   Carver cw;

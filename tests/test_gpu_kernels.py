@@ -27,7 +27,7 @@ def _run_block0(name, prec):
     R, N, D, H, dh = cfg.K, cfg.N, cfg.D, cfg.heads, cfg.dh
     h1 = host(m.residual(dev(x), t, 1))
     ldv = m.info["vt_ld"]
-    assert ldv % 16 == 0 and ldv >= N
+    assert ldv % 64 == 0 and ldv >= N
     # column of each key: the head-dim-64 bf16 layout swaps bits 2 and 3 of the key index
     tok = np.arange(N)
     col = (tok & ~12) | ((tok & 4) << 1) | ((tok & 8) >> 1) if m.info["vt_key_perm"] else tok
