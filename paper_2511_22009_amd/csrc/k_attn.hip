@@ -49,7 +49,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   bf16* const Vs = Ks + 2 * 2 * KT;              // [buf][half][VROWS][VLD]
   const int SPARE = (TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) / 2;  // bf16 index
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qg = wave & 1, kh = wave >> 1;
   const int l32 = lane & 31, g = lane >> 5;
   // Workgroup b runs on XCD b % 8. Give each XCD a contiguous range of (row, head,
@@ -85,20 +85,20 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 
   // staging map, fixed per thread: K chunk c = (key 0..63, 16-byte column); V^T chunk
   // c = (dh row, 8-key column group 0..7). Chunks past the real count read zeros and
-  // land in the spare slot.
+  // land in the spare slot. Each step's loads go through buffer resources based at the
+  // step's first key, so the offsets stay fixed: keys past Nk fall outside the K
+  // resource and read zeros, and the V^T rows (ldv a multiple of 64) hold every key
+  // column a step can reach, zero past the last key.
   const int dh8 = dh >> 3;
   const int kchunks = 2 * kKH * dh8;
   const int vchunks = dh * (2 * kKH / 8);
-  const __amdgpu_buffer_rsrc_t k_src = buffer_rsrc(Kg, (uint32_t)a.Nk * dh * 2);
-  const __amdgpu_buffer_rsrc_t v_src = buffer_rsrc(Vt, (uint32_t)dh * a.ldv * 2);
-  int k_key[KCH], k_goff[KCH], k_lds[KCH], v_key[VCH], v_goff[VCH], v_lds[VCH];
+  int k_goff[KCH], k_lds[KCH], v_goff[VCH], v_lds[VCH];
 #pragma unroll
   for (int i = 0; i < KCH; ++i) {
     const int c = tid + i * 256;
     const bool in = c < kchunks;
     const int key = in ? c / dh8 : 0, col = in ? (c - key * dh8) * 8 : 0;
-    k_key[i] = in ? key : 1 << 24;
-    k_goff[i] = (key * dh + col) * 2;
+    k_goff[i] = in ? (key * dh + col) * 2 : kOffOOB;
     k_lds[i] = in ? (key >> 5) * KT + (key & 31) * KLD + col : -1;
   }
 #pragma unroll
@@ -106,18 +106,17 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     const int c = tid + i * 256;
     const bool in = c < vchunks;
     const int d = in ? c >> 3 : 0, kg = c & 7;
-    v_key[i] = in ? kg * 8 : 1 << 24;
-    v_goff[i] = (d * a.ldv + kg * 8) * 2;
+    v_goff[i] = in ? (d * a.ldv + kg * 8) * 2 : kOffOOB;
     v_lds[i] = in ? (kg >> 2) * VT + d * VLD + (kg & 3) * 8 : -1;
   }
   u32x4 rk[KCH], rv[VCH];
   auto gload = [&](int kv0) {
+    const __amdgpu_buffer_rsrc_t k_src = buffer_rsrc(Kg + (size_t)kv0 * dh, (uint32_t)max(a.Nk - kv0, 0) * dh * 2);
+    const __amdgpu_buffer_rsrc_t v_src = buffer_rsrc(Vt + kv0, (uint32_t)max(dh * a.ldv - kv0, 0) * 2);
 #pragma unroll
-    for (int i = 0; i < KCH; ++i)
-      rk[i] = buffer_load16(k_src, kv0 + k_key[i] < a.Nk ? k_goff[i] + kv0 * dh * 2 : kOffOOB);
+    for (int i = 0; i < KCH; ++i) rk[i] = buffer_load16(k_src, k_goff[i]);
 #pragma unroll
-    for (int i = 0; i < VCH; ++i)
-      rv[i] = buffer_load16(v_src, kv0 + v_key[i] < a.ldv ? v_goff[i] + kv0 * 2 : kOffOOB);
+    for (int i = 0; i < VCH; ++i) rv[i] = buffer_load16(v_src, v_goff[i]);
   };
   auto lstore = [&](int buf) {
     // the chunk counts depend on dh at run time, so every chunk checks its slot
@@ -503,9 +502,9 @@ static void launch_bf16_inst(const AttnArgs& a, hipStream_t s) {
 
 hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
   if (!attention_supports(a.dh)) return hipErrorInvalidValue;
-  // the bf16 kernels read transposed v in the permuted key layout only, the fp32 kernel
-  // in the plain one
-  if ((a.vperm != 0) != use_bf16 || (a.vperm && a.ldv % 16 != 0)) return hipErrorInvalidValue;
+  // the bf16 kernels read transposed v in the permuted key layout only, with rows of
+  // whole 64-key steps; the fp32 kernel reads the plain layout
+  if ((a.vperm != 0) != use_bf16 || (a.vperm && a.ldv % 64 != 0)) return hipErrorInvalidValue;
   if (use_bf16) {
     const int dhc = (a.dh + 15) / 16;
     switch (dhc) {
@@ -513,7 +512,7 @@ hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
       case 2: launch_bf16_inst<2, 1>(a, s); break;
       case 3: launch_bf16_inst<3, 2>(a, s); break;
       case 4:
-        if (a.dh == 64 && a.ldv % 64 == 0)
+        if (a.dh == 64)
           launch(attn_bf16_dma64_kernel, dim3(((a.Nq + kQB - 1) / kQB) * a.heads * a.rows), dim3(256), 0, s, a);
         else
           launch_bf16_inst<4, 2>(a, s);
