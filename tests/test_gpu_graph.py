@@ -136,3 +136,45 @@ def test_modulation_cache_is_bit_identical(graphs):
     for (xa, da), (xb, db) in zip(*runs):
         np.testing.assert_array_equal(xa, xb)
         np.testing.assert_array_equal(da, db)
+
+
+def test_modulation_cache_guided_and_mixed_calls():
+    """With guidance (cond and uncond rows share their latent's table row) and with
+    velocity calls, stream steps of another batch size and a call on another stream
+    interleaved, the cached table is reused only when it is right: every call equals
+    the same call on a model without the cache, bit for bit."""
+    from paper_2511_22009_amd import Cond
+    cfg = W.get_config("tiny_cfg")
+    t, dt = W.slot_times(cfg)
+    K = cfg.K
+    x0 = W.latents(cfg, K)
+    cond = Cond(dev(W.context(cfg, K)), dev(W.null_context(cfg)), cfg.guidance)
+    z = dev(W.z_new_for_image(cfg, 3))
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    # (kind, batch, stream): velocity or stream step
+    calls = [("v", K, s1), ("v", K, s1), ("step", K, s1), ("v", K - 1, s1), ("v", K - 1, s1),
+             ("v", K - 1, s2), ("step", K, s1), ("step", K, s1)]
+    runs = []
+    for cache in (False, True):
+        m = _fresh("tiny_cfg", "bf16")
+        m.modulation_cache(cache)
+        x = dev(x0)
+        d = torch.empty(cfg.latent_shape, device="cuda")
+        res = []
+        for kind, b, st in calls:
+            cb = Cond(cond.ctx[:b], cond.null_ctx, cond.guidance)
+            if kind == "v":
+                out = m.velocity(x[:b], t[:b], cb, stream=st)
+            else:
+                m.stream_step(x, t, dt, b, z, d, cb, stream=st)
+                out = x
+            st.synchronize()
+            res.append(host(out))
+        # reuses: call 2 (same t as call 1), call 3 (same t, a step), call 5 (same t[:K-1]),
+        # call 8 (same t as call 7); not call 6 (another stream) nor call 7 (after a
+        # different batch on another stream)
+        assert m.modulation_cache_stats() == (4 if cache else 0)
+        runs.append(res)
+        m.close()
+    for a, b in zip(*runs):
+        np.testing.assert_array_equal(a, b)
