@@ -48,7 +48,7 @@ __global__ __launch_bounds__(256) void euler_shift_kernel(EulerArgs a) {
 #pragma clang fp contract(off)
   __shared__ float coef[2][kMaxRows];
   if (a.windows > 0) {
-    if (threadIdx.x < a.B) window_coeffs(a, threadIdx.x, &coef[0][threadIdx.x], &coef[1][threadIdx.x]);
+    if ((int)threadIdx.x < a.B) window_coeffs(a, threadIdx.x, &coef[0][threadIdx.x], &coef[1][threadIdx.x]);
     __syncthreads();
   }
   const int e4 = blockIdx.x * blockDim.x + threadIdx.x;

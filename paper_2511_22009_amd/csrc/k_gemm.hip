@@ -888,16 +888,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 #define SF_GEMM_DMA_TILES(X)           \
   X(7, 128, 96, 64, 4, 1, 2, 4)
 
-struct TileInfo {
-  int bm, bn, waves;
-};
-static const TileInfo kTiles[] = {
-#define SF_TILE_INFO(id, bm, bn, bk, wm, wn, ks) {bm, bn, wm * wn * ks},
-    SF_GEMM_TILES(SF_TILE_INFO)
-#undef SF_TILE_INFO
-};
-constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
-
 template <EpiKind KIND>
 static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
   switch (tile) {
