@@ -133,9 +133,10 @@ hipError_t launch_ln(bool out_bf16, const LnArgs& a, hipStream_t s) {
 
 // Four token rows per wavefront. Every load of the rows and of their final
 // shift/scale entries is issued before the first reduction; the linear map D -> P then
-// runs in groups of four outputs: the lane's slice of four W_f rows (read from L2) is
-// applied to all four rows, and the 16 row x output sums leave through one butterfly
-// reduction. The result is written straight to its unpatchified position.
+// runs in groups of four outputs: the lane's slice of four W_f rows (read from L2, the
+// next group's while this one is used) is applied to all four rows, and the 16 row x
+// output sums leave through one butterfly reduction. The result is written straight to
+// its unpatchified position.
 template <int NV>
 __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
   constexpr int RH = 4;
@@ -191,8 +192,9 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
     }
   }
   const int gwn = a.W / a.p;
-  for (int o0 = 0; o0 < a.P; o0 += 4) {
-    float4 w[4][NV];
+  // output groups of four, with the next group's weight rows loaded while this group's
+  // dot products run (two register sets, the loop unrolled by two)
+  auto load_w = [&](float4 (&w)[4][NV], int o0) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const float* wr = a.W_f + (size_t)min(o0 + q, a.P - 1) * a.D;
@@ -202,6 +204,8 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
         w[q][i] = *(const float4*)(wr + 4 * (c < nv ? c : 0));
       }
     }
+  };
+  auto group = [&](const float4 (&w)[4][NV], int o0) {
     float acc[16];
 #pragma unroll
     for (int r = 0; r < RH; ++r)
@@ -224,6 +228,16 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
       const int c = f % a.C, ij = f / a.C;
       const int i = ij / a.p, j = ij - i * a.p;
       a.v[(((size_t)row * a.C + c) * a.H + gh * a.p + i) * a.W + gw * a.p + j] = tot + a.b_f[f];
+    }
+  };
+  float4 wa[4][NV], wb[4][NV];
+  load_w(wa, 0);
+  for (int o0 = 0; o0 < a.P; o0 += 8) {
+    if (o0 + 4 < a.P) load_w(wb, o0 + 4);
+    group(wa, o0);
+    if (o0 + 4 < a.P) {
+      if (o0 + 8 < a.P) load_w(wa, o0 + 8);
+      group(wb, o0 + 4);
     }
   }
 }
