@@ -30,7 +30,11 @@ constexpr int kKH = 32;    // keys per half per step
 constexpr int kQB = 64;    // queries per workgroup
 constexpr float kLazy = 8.0f;  // max drift (exp2 units) tolerated before a rescale
 
-template <int DHC, int DB>  // DHC = ceil(dh/16) contraction chunks, DB = ceil(dh/32) dh blocks
+// DHC = ceil(dh/16) contraction chunks, DB = ceil(dh/32) dh blocks. SUMROW (dh not a
+// multiple of 32, so the last dh block has zero rows): row DB*32 - 8 of every V^T tile
+// is all ones, and the P.V MFMAs then also produce each query's probability sum in that
+// output row, which replaces the per-score additions of the row sum.
+template <int DHC, int DB, bool SUMROW>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   constexpr int KLD = DHC * 16 + 8;     // K tile row pitch (bf16)
   constexpr int VLD = kKH + 8;          // V^T tile row pitch (bf16)
@@ -135,7 +139,16 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const float sl2 = a.scale * 1.4426950408889634f;  // scores -> exp2 units
 
   const int nsteps = (a.Nk + 2 * kKH - 1) / (2 * kKH);
+  constexpr int kSumRow = DB * 32 - 8;
   __syncthreads();
+  if constexpr (SUMROW) {
+    // after the zero fill (the barrier above), before the first tile: the ones row of
+    // both buffers and key halves (never written by the staging, which fills rows < dh)
+    for (int i = tid; i < 2 * 2 * (kKH / 8); i += 256) {
+      const int bhalf = i / (kKH / 8), c = i - bhalf * (kKH / 8);
+      *(u32x4*)&Vs[bhalf * VT + kSumRow * VLD + c * 8] = u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+    }
+  }
   gload(0);
   lstore(0);
   __syncthreads();
@@ -181,7 +194,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const float p = __builtin_amdgcn_exp2f(fmaf(s[ks * 8 + j], sl2, -m2));
-        lsum += p;
+        if constexpr (!SUMROW) lsum += p;
         pf[ks][j] = (bf16)p;
       }
     }
@@ -199,6 +212,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     __syncthreads();
   }
 
+  // the ones row's output (row kSumRow of the last block: register 12 of lane half 0;
+  // lane half 1 holds row kSumRow + 4, a zero row) is this wavefront's probability sum
+  if constexpr (SUMROW) lsum = o[DB - 1][12];
   // merge the key halves: half 1 hands (o, max, partial sum) to half 0 through LDS
   float* mg = (float*)smem + qg * 64 * (DB * 16 + 2);
   if (kh == 1) {
@@ -497,7 +513,10 @@ bool attention_supports(int dh) { return dh >= 8 && dh <= 128 && dh % 8 == 0; }
 template <int DHC, int DB>
 static void launch_bf16_inst(const AttnArgs& a, hipStream_t s) {
   dim3 grid(((a.Nq + kQB - 1) / kQB) * a.heads * a.rows);
-  launch((attn_bf16_kernel<DHC, DB>), grid, dim3(256), 0, s, a);
+  if (a.dh % 32 != 0)
+    launch((attn_bf16_kernel<DHC, DB, true>), grid, dim3(256), 0, s, a);
+  else
+    launch((attn_bf16_kernel<DHC, DB, false>), grid, dim3(256), 0, s, a);
 }
 
 hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
