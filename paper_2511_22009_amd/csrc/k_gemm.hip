@@ -249,13 +249,12 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
     }
   }
   if constexpr (KIND == EPI_QKV) {
-    // transposed v, skipped unless the tile reaches the v columns. Item = (column, RG
-    // consecutive rows): 8 rows, one 16-byte store, in the plain layout; 16 rows, two
-    // 16-byte stores of the permuted key order, in the vt_pos layout (a whole group of
-    // 16 keys). Items that end a network row early or start unaligned go element-wise.
+    // transposed v, skipped unless the tile reaches the v columns. Plain layout: item =
+    // (column, 8 consecutive rows), one 16-byte store. Items that end a network row early
+    // or start unaligned go element-wise.
     if (a.which_base + (int)fdiv((uint32_t)min(n0 + BN, a.N) - 1, a.div_D) < 2) return;
-    auto v_items = [&](auto rg) {
-      constexpr int RG = decltype(rg)::value;
+    auto v_items = [&]() {
+      constexpr int RG = 8;
       constexpr int VT = BM / RG * BN;
       constexpr int VIT = (VT + NT - 1) / NT;
       for (int it = 0; it < VIT; ++it) {
@@ -273,39 +272,70 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
         const bf16* cp = Cs + (rb * RG) * CPB + col;
         bf16* vt = (bf16*)a.vT + (((size_t)r * a.heads + head) * a.dh + d) * a.ldv;
         if (tok + RG <= a.ntok && m + RG <= a.M && (tok & (RG - 1)) == 0) {
-          if constexpr (RG == 8) {
-            bf16x8 o;
+          bf16x8 o;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) o[e] = cp[e * CPB];
-            *(bf16x8*)(vt + tok) = o;
-          } else {
-            // columns tok .. tok+7 hold keys +0..3, +8..11; tok+8 .. tok+15 keys +4..7, +12..15
-            bf16x8 lo, hi;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              lo[e] = cp[e * CPB];
-              lo[4 + e] = cp[(8 + e) * CPB];
-              hi[e] = cp[(4 + e) * CPB];
-              hi[4 + e] = cp[(12 + e) * CPB];
-            }
-            *(bf16x8*)(vt + tok) = lo;
-            *(bf16x8*)(vt + tok + 8) = hi;
-          }
+          for (int e = 0; e < 8; ++e) o[e] = cp[e * CPB];
+          *(bf16x8*)(vt + tok) = o;
         } else {
           for (int e = 0; e < RG && m + e < a.M; ++e) {
             const int me = m + e;
             const int re = (int)fdiv((uint32_t)me, a.div_ntok);
             const int te = me - re * a.ntok;
-            ((bf16*)a.vT)[(((size_t)re * a.heads + head) * a.dh + d) * a.ldv + (a.vperm ? vt_pos(te) : te)] =
+            ((bf16*)a.vT)[(((size_t)re * a.heads + head) * a.dh + d) * a.ldv + te] =
                 cp[e * CPB];
           }
         }
       }
     };
+    // permuted layout: item = (8 adjacent columns, 16 consecutive rows). The 16 rows come
+    // from LDS as one 16-byte read each and are transposed in registers (two bf16 per
+    // v_perm); each column leaves as two 16-byte stores in the permuted key order.
+    auto v_items_perm = [&]() {
+      constexpr int CG = BN / 8;
+      constexpr int VT = BM / 16 * CG;
+      constexpr int VIT = (VT + NT - 1) / NT;
+      for (int it = 0; it < VIT; ++it) {
+        const int c = tid + it * NT;
+        const int rb = c / CG, cg = c - rb * CG;  // adjacent lanes: adjacent column groups
+        const int n = n0 + cg * 8, m = m0 + rb * 16;
+        if ((VT % NT != 0 && c >= VT) || n >= a.N || m >= a.M) continue;
+        const int part = (int)fdiv((uint32_t)n, a.div_D);
+        if (a.which_base + part < 2) continue;
+        const int rem = n - part * a.D;
+        const int head = (int)fdiv((uint32_t)rem, a.div_dh);
+        const int d0 = rem - head * a.dh;  // the 8 columns are dims d0.. of one head (dh % 8 == 0)
+        const int r = (int)fdiv((uint32_t)m, a.div_ntok);
+        const int tok = m - r * a.ntok;
+        if (tok + 16 <= a.ntok && m + 16 <= a.M && (tok & 15) == 0 && n + 8 <= a.N) {
+          u32x4 rows[16];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) rows[e] = *(const u32x4*)&Cs[(rb * 16 + e) * CPB + cg * 8];
+          bf16* vt = (bf16*)a.vT + (((size_t)r * a.heads + head) * a.dh + d0) * a.ldv + tok;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            // column j: bf16 j of every row; a word packs tokens (t0, t1) low to high
+            const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+            auto pk = [&](int t0, int t1) { return __builtin_amdgcn_perm(rows[t1][j >> 1], rows[t0][j >> 1], sel); };
+            // key columns tok..tok+7 hold keys 0-3, 8-11; tok+8..tok+15 keys 4-7, 12-15
+            *(u32x4*)(vt + (size_t)j * a.ldv) = u32x4{pk(0, 1), pk(2, 3), pk(8, 9), pk(10, 11)};
+            *(u32x4*)(vt + (size_t)j * a.ldv + 8) = u32x4{pk(4, 5), pk(6, 7), pk(12, 13), pk(14, 15)};
+          }
+        } else {
+          for (int e = 0; e < 16 && m + e < a.M; ++e) {
+            const int me = m + e;
+            const int re = (int)fdiv((uint32_t)me, a.div_ntok);
+            const int te = me - re * a.ntok;
+            for (int j = 0; j < 8 && n + j < a.N; ++j)
+              ((bf16*)a.vT)[(((size_t)re * a.heads + head) * a.dh + d0 + j) * a.ldv + vt_pos(te)] =
+                  Cs[(rb * 16 + e) * CPB + cg * 8 + j];
+          }
+        }
+      }
+    };
     if (a.vperm)
-      v_items(std::integral_constant<int, 16>{});
+      v_items_perm();
     else
-      v_items(std::integral_constant<int, 8>{});
+      v_items();
   }
 }
 
