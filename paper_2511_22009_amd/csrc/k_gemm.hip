@@ -911,8 +911,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   X(0, 128, 128, 64, 2, 2, 1)     \
   X(1, 128, 288, 64, 2, 3, 1)     \
   X(2, 128, 384, 64, 2, 4, 1)     \
-  X(6, 128, 128, 128, 2, 2, 2)     \
-  X(3, 256, 192, 64, 4, 2, 1)
+  X(6, 128, 128, 128, 2, 2, 2)
 
 // Directly staged tiles (as above, plus the number of LDS stages).
 #define SF_GEMM_DMA_TILES(X)           \
@@ -954,10 +953,8 @@ static hipError_t launch_bf16_tile(int tile, const GemmArgs& a, hipStream_t s) {
 // how many rows are in the batch. Otherwise 128x128 (64x64 per wavefront) is the
 // general tile; 128x384 and 128x288 (64x96 per wavefront, 8 and 6 wavefronts) win when
 // they cut the problem into exactly one workgroup per CU (e.g. 4096x3072 and
-// 4096x2304), and 256x192 (64x96 per wavefront, 8 wavefronts) when its tiles fill whole
-// rounds of 256 workgroups (e.g. 16384x4608, the 1024^2 MLP up-projection: 184 us
-// against 192 for 128x128); these four accumulate in the same order, so switching among
-// them with M changes no result bit.
+// 4096x2304); these three accumulate in the same order, so switching among them with M
+// changes no result bit.
 int choose_gemm_tile(int M, int N, int K) {
   (void)K;
   if (N % 96 == 0 && N <= 768) return 7;
@@ -965,7 +962,6 @@ int choose_gemm_tile(int M, int N, int K) {
   auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
   if (M % 128 == 0 && N % 384 == 0 && tiles(128, 384) == 256) return 2;
   if (M % 128 == 0 && N % 288 == 0 && tiles(128, 288) == 256) return 1;
-  if (M % 256 == 0 && N % 192 == 0 && tiles(256, 192) % 256 == 0) return 3;
   return 0;
 }
 
