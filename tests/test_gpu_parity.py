@@ -316,3 +316,55 @@ def test_one_step_queue_matches_oracle(prec):
     ref = oracle.run_stream(oracle_model("tiny_tsens"), grid, 3, lambda j: W.z_new_for_image(cfg, j))
     for i in range(3):
         assert rel_l2(host(imgs[i]), ref[i]) <= TOL[prec]
+
+
+# ------------------------------------------------------------------ batch limits
+
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("name", ["ragged", "dh64"])
+def test_max_rows_velocity_parity(name, prec):
+    """The largest batch one call takes (64 network rows, the ABI's limit), every sample at
+    its own t: Eq. 5's heterogeneous call against the oracle, sample by sample."""
+    cfg = W.get_config(name)
+    B = 64
+    x = W.latents(cfg, B, seed=71)
+    t = np.random.default_rng(72).uniform(0.0, 1.0, B).astype(np.float32)
+    ref = oracle.velocity(oracle_model(name), x, t)
+    got = host(model(name, prec, max_rows=B).velocity(dev(x), t))
+    errs = [rel_l2(got[k], ref[k]) for k in range(B)]
+    assert max(errs) <= TOL[prec], max(errs)
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_max_rows_guided_velocity_parity(prec):
+    """32 text-conditioned samples with guidance fill all 64 rows (cond and uncond)."""
+    from paper_2511_22009_amd import Cond
+    cfg = W.get_config("tiny_cfg")
+    B = 32
+    x = W.latents(cfg, B, seed=73)
+    t = np.random.default_rng(74).uniform(0.0, 1.0, B).astype(np.float32)
+    ctx, nctx = W.context(cfg, B), W.null_context(cfg)
+    ref = oracle.velocity(oracle_model("tiny_cfg"), x, t, ctx, nctx, cfg.guidance)
+    m = model("tiny_cfg", prec, max_rows=2 * B)
+    got = host(m.velocity(dev(x), t, Cond(dev(ctx), dev(nctx), cfg.guidance)))
+    errs = [rel_l2(got[k], ref[k]) for k in range(B)]
+    assert max(errs) <= TOL[prec], max(errs)
+
+
+def test_batch_beyond_capacity_is_rejected():
+    """A call needing more network rows than the model was loaded for fails with an error
+    and writes nothing; guidance doubles the rows a sample needs."""
+    from paper_2511_22009_amd import Cond, SFError
+    cfg = W.get_config("tiny_cfg")
+    m = model("tiny_cfg", "bf16", max_rows=4)
+    x = dev(W.latents(cfg, 5))
+    t = np.full(5, 0.5, np.float32)
+    out = torch.full((5,) + cfg.latent_shape, 7.0, device="cuda")
+    with pytest.raises(SFError):
+        m.velocity(x, t, out=out)
+    cond = Cond(dev(W.context(cfg, 3)), dev(W.null_context(cfg)), cfg.guidance)
+    with pytest.raises(SFError):
+        m.velocity(x[:3], t[:3], cond, out=out[:3])
+    assert bool((host(out) == 7.0).all())
+    ok = host(m.velocity(x[:2], t[:2], Cond(dev(W.context(cfg, 2)), dev(W.null_context(cfg)), cfg.guidance)))
+    assert np.isfinite(ok).all()
