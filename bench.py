@@ -46,9 +46,9 @@ MI355X_HBM_GBS = 8000.0
 # only for the kernel sources it was measured on (hash below); otherwise traffic is null.
 KERNEL_SOURCES = ("k_gemm.hip", "sf_device.h", "sf_launch.h")
 TRAFFIC = {
-    ("s512", "bf16", "FC2"): {"bytes": 94526902, "sources": "b7d6034152cfe5e9",
+    ("s512", "bf16", "FC2"): {"bytes": 94526902, "sources": "06e72fb95d785882",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512", "bf16", "FC1"): {"bytes": 56844131, "sources": "b7d6034152cfe5e9",
+    ("s512", "bf16", "FC1"): {"bytes": 56844131, "sources": "06e72fb95d785882",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
 }
 

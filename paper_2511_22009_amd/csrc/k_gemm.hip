@@ -8,7 +8,7 @@
 //   RES      h += acc + bias.
 //
 // bf16 path: v_mfma_f32_32x32x16_bf16 on BM x BN x BK workgroup tiles (BK 64 or 128;
-// table at the end), each wavefront owning a 64x64 or 64x96 sub-tile, optionally with
+// table at the end), each wavefront owning a 64x64, 64x96 or 32x96 sub-tile, optionally with
 // the K slice split over two sets of wavefronts; both operand tiles are
 // double-buffered in LDS with a 16-byte row pad so the 16-byte fragment reads of a
 // 32-lane column are free of bank conflicts, and the next K-slice is fetched into
