@@ -201,6 +201,34 @@ def test_constant_field_stream_closed_form(prec):
     m.close()
 
 
+def test_alg2_driver_network_call_count():
+    """Eq. 7 on the GPU driver: M images take M + K - 1 network calls, the first K - 1 at
+    occupancy 1 .. K - 1 with nothing finished, then M at occupancy K, each emitting one
+    finished latent."""
+    from paper_2511_22009_amd.pipeline import run_images
+    cfg = W.get_config("tiny")
+    inner = model("tiny", "bf16")
+
+    class Counting:
+        def __init__(self):
+            self.calls = []
+
+        def __getattr__(self, name):
+            return getattr(inner, name)
+
+        def stream_step(self, x, t, dt, B, z_new, x_done=None, cond=None, stream=None):
+            self.calls.append((B, x_done is not None))
+            return inner.stream_step(x, t, dt, B, z_new, x_done, cond, stream)
+
+    m = Counting()
+    grid = W.schedule(cfg)
+    K, M = len(grid) - 1, 6
+    imgs = run_images(m, grid, M, lambda j: dev(W.z_new_for_image(cfg, j)))
+    assert len(imgs) == M and len(m.calls) == M + K - 1
+    assert m.calls == [(b, False) for b in range(1, K)] + [(K, True)] * M
+    assert all(np.isfinite(host(i)).all() for i in imgs)
+
+
 @pytest.mark.parametrize("prec", PRECS)
 def test_stream_equals_sequential_on_gpu(prec):
     """Alg. 2 through sf_stream_step (fill, then full) gives each image exactly what
