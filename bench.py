@@ -114,7 +114,35 @@ def cpu_baseline(cfg, budget_s=12.0):
     threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
     return {"value": cfg.K * steps / el, "unit": "latent-steps/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{steps} full stream step(s) of the {cfg.name} workload ({cfg.K} latents each), "
-                      f"NumPy fp32, {el:.1f} s"}
+                      f"NumPy fp32, {el:.1f} s",
+            "single_thread": single_thread_baseline(cfg, m, x, t, dt, kw)}
+
+
+def single_thread_baseline(cfg, m, x, t, dt, kw):
+    """The oracle on ONE host thread: the bench workload on a bounded sample (one
+    latent's network call and Euler update, i.e. one latent-step) and Tiny over 100
+    full stream steps."""
+    import oracle
+    from threadpoolctl import threadpool_limits
+    out = {}
+    with threadpool_limits(limits=1):
+        one_kw = {k: (v[:1] if k == "ctx" else v) for k, v in kw.items()}
+        t0 = time.perf_counter()
+        oracle.stream_step(m, x[:1], t[:1], dt[:1], x[0], **one_kw)
+        el = time.perf_counter() - t0
+        out[cfg.name] = {"value": 1.0 / el, "unit": "latent-steps/s", "cores": 1,
+                         "sample": f"one latent-step of the {cfg.name} workload, {el:.1f} s"}
+        tiny = W.get_config("tiny")
+        tm = oracle.load_blob(W.make_blob(tiny))
+        tt, tdt = W.slot_times(tiny)
+        tx = W.latents(tiny, tiny.K)
+        t0 = time.perf_counter()
+        for _ in range(100):
+            tx, _, _ = oracle.stream_step(tm, tx, tt, tdt, tx[0])
+        el = time.perf_counter() - t0
+        out["tiny"] = {"value": tiny.K * 100 / el, "unit": "latent-steps/s", "cores": 1,
+                       "sample": f"100 full stream steps of the tiny workload ({tiny.K} latents each), {el:.2f} s"}
+    return out
 
 
 def main():

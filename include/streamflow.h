@@ -99,9 +99,11 @@ typedef struct sf_info {
  * `blob` is a HOST pointer; it is read during the call and not retained. On success
  * *out owns device memory until sf_free. Errors: SF_E_INVAL (null blob/out, bad
  * precision or max_rows), SF_E_BLOB, SF_E_UNSUPPORTED (head dim not a multiple of 8
- * or above 128, a width not a multiple of 8, H or W not a multiple of p), SF_E_OOM,
- * SF_E_HIP. The environment variable SF_FAIL_ALLOC_AFTER=n makes the (n+1)-th device
- * allocation of a load fail, to exercise the SF_E_OOM path. */
+ * or above 128, a width not a multiple of 8, H or W not a multiple of p; in bf16 mode
+ * an activation of max_rows rows reaching 2^31 bytes, e.g. max_rows x tokens x the MLP
+ * width x 2, since the bf16 kernels use 32-bit byte offsets), SF_E_OOM, SF_E_HIP. No
+ * handle is returned on failure. The environment variable SF_FAIL_ALLOC_AFTER=n makes
+ * the (n+1)-th device allocation of a load fail, to exercise the SF_E_OOM path. */
 int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows, sf_model** out);
 
 /* Release everything the handle owns. NULL is a no-op. Waits for the device. */
@@ -217,7 +219,9 @@ typedef struct {
 /* Set (p != NULL) or clear (p == NULL: Euler on the velocity, the default) the
  * scheduler of sf_stream_step and sf_scheduler_shift. Synchronous: builds the schedule
  * on the host in fp64 and uploads it (one device allocation, kept until sf_free).
- * Drops cached graphs. SF_E_INVAL on out-of-range fields. */
+ * Drops cached graphs. SF_E_INVAL on out-of-range fields. On SF_E_OOM or SF_E_HIP the
+ * scheduler is cleared (Euler on the velocity), never left half set. The schedule's
+ * allocation fails when SF_FAIL_ALLOC_AFTER is 0, to exercise that path. */
 int sf_set_scheduler(sf_model* m, const sf_perflow* p);
 
 /* The update and shift of sf_stream_step alone, with the model's scheduler, for a

@@ -158,54 +158,58 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     if (it + 1 < nsteps) gload((it + 1) * 2 * kKH);
     const bf16* Kb = Ks + (cur * 2 + kh) * KT;
     const bf16* Vb = Vs + (cur * 2 + kh) * VT;
-
-    f32x16 s;
+    // a key half that lies wholly past the last key (key half 1 when Nk <= 32, or the
+    // tail of the last step) contributes nothing: its scores would all be -inf, and a
+    // wavefront that has seen no key yet would take exp2(-inf + inf)
+    if (kv0 < a.Nk) {
+      f32x16 s;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) s[e] = 0.0f;
+      for (int e = 0; e < 16; ++e) s[e] = 0.0f;
 #pragma unroll
-    for (int kk = 0; kk < DHC; ++kk) {
-      const bf16x8 kf = *(const bf16x8*)&Kb[l32 * KLD + kk * 16 + g * 8];
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
-    }
-    // s[e]: query l32, key kv0 + (e/4)*8 + g*4 + e%4, raw (unscaled). Only the last,
-    // ragged step needs the key mask.
-    if (kv0 + kKH > a.Nk) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e)
-        if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) s[e] = -INFINITY;
-    }
-    float tmax = s[0];
-#pragma unroll
-    for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, s[e]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
-    if (__any(tmax > m2 + kLazy)) {
-      const float mnew = fmaxf(m2, tmax);
-      const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
-      lsum *= alpha;
-#pragma unroll
-      for (int b = 0; b < DB; ++b)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
-      m2 = mnew;
-    }
-    bf16x8 pf[2];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[ks * 8 + j], sl2, -m2));
-        if constexpr (!SUMROW) lsum += p;
-        pf[ks][j] = (bf16)p;
+      for (int kk = 0; kk < DHC; ++kk) {
+        const bf16x8 kf = *(const bf16x8*)&Kb[l32 * KLD + kk * 16 + g * 8];
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
       }
-    }
-    // V^T fragment of k-slots 8g..8g+7 (keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
-    // of this half): one 16-byte read in the permuted key layout (vt_pos)
+      // s[e]: query l32, key kv0 + (e/4)*8 + g*4 + e%4, raw (unscaled). Only the last,
+      // ragged step needs the key mask.
+      if (kv0 + kKH > a.Nk) {
 #pragma unroll
-    for (int b = 0; b < DB; ++b) {
+        for (int e = 0; e < 16; ++e)
+          if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) s[e] = -INFINITY;
+      }
+      float tmax = s[0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, s[e]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+      if (__any(tmax > m2 + kLazy)) {
+        const float mnew = fmaxf(m2, tmax);
+        const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
+        lsum *= alpha;
+#pragma unroll
+        for (int b = 0; b < DB; ++b)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
+        m2 = mnew;
+      }
+      bf16x8 pf[2];
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const bf16x8 vf = *(const bf16x8*)&Vb[(b * 32 + l32) * VLD + ks * 16 + g * 8];
-        o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[ks * 8 + j], sl2, -m2));
+          if constexpr (!SUMROW) lsum += p;
+          pf[ks][j] = (bf16)p;
+        }
+      }
+      // V^T fragment of k-slots 8g..8g+7 (keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
+      // of this half): one 16-byte read in the permuted key layout (vt_pos)
+#pragma unroll
+      for (int b = 0; b < DB; ++b) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const bf16x8 vf = *(const bf16x8*)&Vb[(b * 32 + l32) * VLD + ks * 16 + g * 8];
+          o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
+        }
       }
     }
     if (it + 1 < nsteps) lstore(cur ^ 1);
@@ -231,7 +235,10 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const float mnew = fmaxf(m2, m2b);
   const float a0 = m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2 - mnew);
   const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
-  lsum = lsum * a0 + mg[(DB * 16 + 1) * 64 + lane] * a1;
+  // a half that saw no key (max still -inf) holds zeros and is left out by selects,
+  // not multiplied by a zero weight
+  const bool own = m2 != -INFINITY, other = m2b != -INFINITY;
+  lsum = (own ? lsum * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
   lsum += __shfl_xor(lsum, 32);
   const float inv = 1.0f / lsum;
   if (qi < a.Nq) {
@@ -245,7 +252,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int e = e4 * 4 + q;
-          w[q] = (o[b][e] * a0 + mg[(b * 16 + e) * 64 + lane] * a1) * inv;
+          w[q] = ((own ? o[b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
         }
         if (d < dh) *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
       }
@@ -350,6 +357,8 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
     issue(stage(std::integral_constant<int, S + kAttnStages - 1>{}), it + kAttnStages - 1);
     const char* cur = stage(std::integral_constant<int, S>{});
     const int kv0 = it * 2 * kKH + kh * kKH;
+    // a key half wholly past the last key contributes nothing (see attn_bf16_kernel)
+    if (kv0 >= a.Nk) return;
     f32x16 sc;
 #pragma unroll
     for (int e = 0; e < 16; ++e) sc[e] = 0.0f;
@@ -433,7 +442,10 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   const float mnew = fmaxf(m2, m2b);
   const float a0 = m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2 - mnew);
   const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
-  lsum = lsum * a0 + mg[(DB * 16 + 1) * 64 + lane] * a1;
+  // a half that saw no key (max still -inf) holds zeros and is left out by selects,
+  // not multiplied by a zero weight
+  const bool own = m2 != -INFINITY, other = m2b != -INFINITY;
+  lsum = (own ? lsum * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
   lsum += __shfl_xor(lsum, 32);
   const float inv = 1.0f / lsum;
   if (qi < a.Nq) {
@@ -447,7 +459,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int e = e4 * 4 + q;
-          w[q] = (o[b][e] * a0 + mg[(b * 16 + e) * 64 + lane] * a1) * inv;
+          w[q] = ((own ? o[b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
         }
         *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
       }

@@ -95,7 +95,8 @@ __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 // Raw buffer resource over [base, base + bytes): a load whose byte offset is at or
 // past `bytes` returns zeros in hardware, so tile loads need no branches.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-constexpr int kOffOOB = 0x7ffffff0;  // any offset >= every buffer size used here
+constexpr int kOffOOB = kOffOOBHost;  // any offset >= every buffer size used here (the
+                                      // loader bounds each operand below it)
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }

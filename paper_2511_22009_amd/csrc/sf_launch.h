@@ -25,6 +25,7 @@ inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t s,
 }
 
 constexpr int kMaxRows = 64;     // equals SF_MAX_ROWS
+constexpr int kOffOOBHost = 0x7ffffff0;  // the device code's past-the-end buffer offset
 constexpr int kMaxWidth = 2048;  // largest D / mlp input width a row kernel holds
 constexpr int kMaxPatch = 32;    // largest p*p*C
 

@@ -162,8 +162,22 @@ int check_supported(const Header& h) {
       h.tdim > (uint32_t)sf::kMaxWidth || P > (uint32_t)sf::kMaxPatch || !sf::attention_supports((int)dh) ||
       (h.C * h.H * h.W) % 4 || (h.has_cross && h.ctx_dim % 8))
     return SF_E_UNSUPPORTED;
+  return SF_OK;
+}
+
+// The bf16 GEMMs and attention address their operands through buffer resources with
+// 32-bit byte offsets (int arithmetic, kOffOOB as the past-the-end sentinel), so every
+// activation operand must stay below kOffOOB bytes at the loaded row count; the fp32
+// kernels index with size_t and are bounded only by the element counts.
+int check_capacity(const Header& h, int max_rows, size_t es) {
   const uint64_t N = (uint64_t)(h.H / h.p) * (h.W / h.p);
-  if (N * sf::kMaxRows * (uint64_t)(h.mlp > h.D ? h.mlp : h.D) >= (1ull << 31)) return SF_E_UNSUPPORTED;
+  const uint64_t R = (uint64_t)max_rows;
+  const uint64_t widest = h.mlp > h.D ? h.mlp : h.D;
+  const uint64_t limit = es == 2 ? (uint64_t)sf::kOffOOBHost : (1ull << 31);
+  const uint64_t unit = es == 2 ? es : 1;  // bytes (bf16) or elements (fp32)
+  if (R * N * widest * unit >= limit) return SF_E_UNSUPPORTED;
+  if (h.has_cross && R * h.ctx_len * (uint64_t)(h.ctx_dim > h.D ? h.ctx_dim : h.D) * unit >= limit)
+    return SF_E_UNSUPPORTED;
   return SF_OK;
 }
 
@@ -648,6 +662,7 @@ int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows
   int rc = check_header(blob, nbytes, &h, &expect);
   if (rc != SF_OK) return rc;
   if ((rc = check_supported(h)) != SF_OK) return rc;
+  if ((rc = check_capacity(h, max_rows, precision == SF_PREC_BF16 ? 2 : 4)) != SF_OK) return rc;
 
   sf_model* m = new (std::nothrow) sf_model();
   if (!m) return SF_E_OOM;
@@ -939,17 +954,24 @@ int sf_set_scheduler(sf_model* m, const sf_perflow* p) {
   }
   if (hipDeviceSynchronize() != hipSuccess) return SF_E_HIP;
   drop_graphs(m);
+  // the scheduler is off until the new schedule is in place: a failure below leaves
+  // Euler on the velocity, never a window count without its schedule
+  m->windows = 0;
   if (m->n_abar != T) {
     if (m->abar) (void)hipFree(m->abar);
     m->abar = nullptr;
     m->n_abar = 0;
-    if (hipMalloc((void**)&m->abar, sizeof(double) * (size_t)T) != hipSuccess) return SF_E_OOM;
+    if (fail_alloc_after() == 0 || hipMalloc((void**)&m->abar, sizeof(double) * (size_t)T) != hipSuccess) {
+      m->abar = nullptr;
+      (void)hipGetLastError();
+      return SF_E_OOM;
+    }
     m->n_abar = T;
   }
   if (hipMemcpy(m->abar, ab.data(), sizeof(double) * (size_t)T, hipMemcpyHostToDevice) != hipSuccess)
     return SF_E_HIP;
-  m->windows = p->windows;
   m->win_eps = p->eps;
+  m->windows = p->windows;
   return SF_OK;
 }
 

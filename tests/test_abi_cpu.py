@@ -91,3 +91,19 @@ def test_strerror_texts():
     texts = {c: L.sf_strerror(c).decode() for c in range(-6, 1)}
     assert texts[0] == "ok" and len(set(texts.values())) == 7
     assert L.sf_strerror(-99).decode() == "unknown status code"
+
+
+def test_load_rejects_rows_whose_operands_pass_the_offset_range():
+    """The bf16 kernels address activations with 32-bit byte offsets: a load whose
+    largest operand (rows x tokens x MLP width, bf16) would reach 2^31 bytes is refused
+    on the host, from the header alone. At 1024^2 (4096 tokens, MLP 4608) 64 rows are
+    2.4 GB; the loader never gets to read past the 64-byte header it is given."""
+    import numpy as np
+    from workloads.blob import HEADER_FMT, MAGIC, VERSION, header_fields, tensor_specs
+    cfg = W.get_config("s1024")
+    head = struct.pack(HEADER_FMT, MAGIC, VERSION, *header_fields(cfg), 0)
+    nbytes = len(head) + 4 * sum(int(np.prod(s)) for _, s in tensor_specs(cfg))
+    assert 64 * cfg.N * cfg.mlp * 2 >= 0x7ffffff0
+    h = ctypes.c_void_p()
+    rc = load_library().sf_load_weights(head, nbytes, 0, 64, ctypes.byref(h))
+    assert rc == -6 and not h.value

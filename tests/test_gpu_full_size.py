@@ -126,3 +126,119 @@ def test_s1024_step_properties():
     np.testing.assert_array_equal(got[0], z)
     np.testing.assert_array_equal(got[1:], expect[:-1])
     np.testing.assert_array_equal(host(done), expect[-1])
+
+
+def test_s1024_full_depth_velocity_parity():
+    """1024^2 (4096 tokens, 28 blocks, head dim 72) through the whole network and the
+    output head, in the benchmark's launch configuration (all K slots in one call):
+    the newest and the oldest slot against the oracle's velocity (the slots between are
+    tied to them by batch invariance, test_s1024_step_properties)."""
+    cfg, x, t, _ = _inputs("s1024")
+    got = host(model("s1024", "bf16", max_rows=cfg.rows).velocity(dev(x), t))
+    om = oracle_model("s1024")
+    errs = {}
+    for k in (0, cfg.K - 1):
+        ref = oracle.forward_one(om, x[k], t[k])
+        errs[k] = rel_l2(got[k], ref)
+    print("s1024 full-depth v relative L2 per slot:", {k: f"{e:.3e}" for k, e in errs.items()})
+    assert max(errs.values()) <= TOL_BF16, errs
+
+
+def test_s512_graph_replay_with_cached_modulation_vs_oracle():
+    """The benchmark's headline execution: steps replayed from captured HIP graphs on a
+    side stream, with the modulation cache on (steady state: every slot keeps its t).
+    Each step's update of every slot against the oracle's stream step from the same
+    state (teacher-forced), over steps that capture, then reuse the table, then replay."""
+    from paper_2511_22009_amd import Model, Precision
+    from conftest import blob_for
+    cfg, x, t, dt = _inputs("s512")
+    om = oracle_model("s512")
+    m = Model(blob_for("s512"), Precision.BF16, cfg.rows)
+    m.graph_enable(True)
+    m.modulation_cache(True)
+    s = torch.cuda.Stream()
+    pool = [dev(W.z_new_for_image(cfg, 40 + i)) for i in range(2)]
+    xd = dev(x)
+    done = torch.empty(cfg.latent_shape, device="cuda")
+    worst = 0.0
+    for step in range(6):
+        before = host(xd)
+        z = pool[step % 2]
+        m.stream_step(xd, t, dt, cfg.K, z, done, stream=s)
+        s.synchronize()
+        got = host(xd)
+        np.testing.assert_array_equal(got[0], host(z))
+        new = np.concatenate([got[1:], host(done)[None]])
+        _, _, v_ref = oracle.stream_step(om, before, t, dt, host(z))
+        errs = [rel_l2(new[k] - before[k], dt[k] * v_ref[k]) for k in range(cfg.K)]
+        worst = max(worst, max(errs))
+        assert max(errs) <= TOL_BF16, (step, errs)
+    cached, replays = m.graph_stats()
+    skips = m.modulation_cache_stats()
+    print(f"s512 replayed + cached-table steps: worst update relative L2 {worst:.3e}, "
+          f"graphs {cached}, replays {replays}, conditioning skips {skips}")
+    assert replays >= 2 and skips >= 5
+    m.close()
+
+
+def _bf16_weights(W_):
+    from helpers import bf16_round
+    return bf16_round(W_).astype(np.float64)
+
+
+def test_s512_kernels_on_their_own_inputs():
+    """Every kernel of block 0 at 512^2 in bf16 (the launch configuration the benchmark
+    times: the 128x288 QKV tile with the permuted transposed-v store, head-dim-64
+    attention with directly staged K/V, the 128x384 fc1 tile with GELU, the directly
+    staged 128x96 out-projection and fc2 tiles with the gated residual) against fp64
+    arithmetic on exactly the inputs that kernel read, element by element:
+    |got - ref| <= rel |ref| + floor rms(ref). rel = 2^-8 is one bf16 rounding of the
+    output (2^-7 where the kernel also rounds an internal operand, the attention
+    probabilities, or where an input of ours may sit one bf16 step off the kernel's)."""
+    from helpers import bf16_round, elementwise_ratio
+    from paper_2511_22009_amd import Buffer
+    cfg, x, t, _ = _inputs("s512")
+    m = model("s512", "bf16", max_rows=cfg.rows)
+    R, N, D, H, dh, F = cfg.K, cfg.N, cfg.D, cfg.heads, cfg.dh, cfg.mlp
+    h0 = host(m.residual(dev(x), t, 0)).astype(np.float64)
+    h1 = host(m.residual(dev(x), t, 1)).astype(np.float64)
+    ldv = m.info["vt_ld"]
+    tok = np.arange(N)
+    col = (tok & ~12) | ((tok & 4) << 1) | ((tok & 8) >> 1)
+    q = host(m.debug_read(Buffer.Q, (R, H, N, dh))).transpose(0, 2, 1, 3).reshape(R, N, D).astype(np.float64)
+    k_ = host(m.debug_read(Buffer.K, (R, H, N, dh))).transpose(0, 2, 1, 3).reshape(R, N, D).astype(np.float64)
+    v = host(m.debug_read(Buffer.VT, (R, H, dh, ldv)))[..., col].transpose(0, 3, 1, 2).reshape(R, N, D)
+    v = v.astype(np.float64)
+    attn = host(m.debug_read(Buffer.ATTN, (R, N, D))).astype(np.float64)
+    ln2 = host(m.debug_read(Buffer.ACT, (R, N, D))).astype(np.float64)
+    mlp = host(m.debug_read(Buffer.MLP, (R, N, F))).astype(np.float64)
+    table = host(m.debug_read(Buffer.TABLE, (R, m.info["mod_width"]))).astype(np.float64)
+    b = oracle_model("s512").blocks[0]
+    Wqkv, Wo, W1, W2 = (_bf16_weights(b[n]) for n in ("W_qkv", "W_o", "W_fc1", "W_fc2"))
+
+    def ln(z):
+        mu = z.mean(-1, keepdims=True)
+        d = z - mu
+        return d / np.sqrt((d * d).mean(-1, keepdims=True) + 1e-6)
+
+    worst = {}
+
+    def check(name, got, ref, rel, floor):
+        r = elementwise_ratio(got, ref, rel, floor)
+        worst[name] = max(worst.get(name, 0.0), r)
+        worst[name + "_relL2"] = max(worst.get(name + "_relL2", 0.0), rel_l2(got, ref))
+
+    for s in range(R):
+        sh1, sc1, g1, sh2, sc2, g2 = table[s, :6 * D].reshape(6, D)
+        a1 = bf16_round(ln(h0[s]) * (1 + sc1) + sh1).astype(np.float64)       # the QKV GEMM's A operand
+        qkv = a1 @ Wqkv.T + b["b_qkv"]
+        check("qkv", np.concatenate([q[s], k_[s], v[s]], 1), qkv, 2.0 ** -7, 2.0 ** -8)
+        check("attention", attn[s], oracle.attention(q[s], k_[s], v[s], H), 2.0 ** -7, 2.0 ** -6)
+        h_mid = h0[s] + g1 * (attn[s] @ Wo.T + b["b_o"])
+        check("ln2", ln2[s], ln(h_mid) * (1 + sc2) + sh2, 2.0 ** -7, 2.0 ** -8)
+        check("fc1_gelu", mlp[s], oracle.gelu_tanh(ln2[s] @ W1.T + b["b_fc1"]), 2.0 ** -8, 2.0 ** -8)
+        check("proj_fc2_residual", h1[s], h_mid + g2 * (mlp[s] @ W2.T + b["b_fc2"]), 1e-5, 1e-5)
+    print("s512 bf16 block-0 kernels on their own inputs (ratio <= 1 passes):",
+          {k: f"{v:.3e}" for k, v in worst.items()})
+    for name in ("qkv", "attention", "ln2", "fc1_gelu", "proj_fc2_residual"):
+        assert worst[name] <= 1.0, (name, worst)

@@ -90,6 +90,14 @@ CONFIGS = {
     # head dim 64 (as in the width-768 nets) with a ragged token count: 300 tokens are
     # five 64-key attention steps, the last holding 44 keys
     "dh64": Config("dh64", C=4, H=20, W=60, p=2, D=128, L=2, heads=2, mlp=512),
+    # at most 32 tokens (or context tokens): a whole attention key half of 32 lies past
+    # the last key. 16 tokens at head dims 32 and 72, 32 tokens at head dim 64, and the
+    # Tiny guided network with contexts of 20 and 32 tokens
+    "short16": Config("short16", C=4, H=8, W=8, p=2, D=128, L=2, heads=4, mlp=512),
+    "short16_dh72": Config("short16_dh72", C=4, H=8, W=8, p=2, D=144, L=2, heads=2, mlp=576),
+    "short32_dh64": Config("short32_dh64", C=4, H=8, W=16, p=2, D=128, L=2, heads=2, mlp=512),
+    "tiny_cfg_ctx20": replace(_TINY, name="tiny_cfg_ctx20", ctx_len=20, ctx_dim=64, has_cross=1, cfg=True),
+    "tiny_cfg_ctx32": replace(_TINY, name="tiny_cfg_ctx32", ctx_len=32, ctx_dim=64, has_cross=1, cfg=True),
     # 512^2 image: 4x64x64 latent, 1024 tokens, width 768, 12 blocks, 12 heads
     "s512": _S512,
     # 512^2, width 1152, 28 blocks, 16 heads; every slot at a different step
