@@ -146,6 +146,18 @@ int sf_euler_shift(sf_model* m, float* x, const float* v, const float* dt, int B
  * gate2) of width D each, then the final layer's (shift, scale). */
 int sf_modulation(sf_model* m, const float* t, int B, float* table, void* hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): sf_modulation with its two
+ * intermediates (the timestep MLP's hidden layer and SiLU(c), [B][D] fp32 each) in a
+ * fixed device array of the library (1 MiB per GPU, allocated with the library's code
+ * object and held until the process ends) instead of the model's workspace. Same
+ * arguments and results as sf_modulation (bit-identical table); B may be 1..SF_MAX_ROWS
+ * regardless of max_rows (SF_E_INVAL beyond: the array holds 2 x 64 x 2048 floats).
+ * Calls no allocating routine. Every call on one GPU uses that GPU's one array, so
+ * calls that overlap on a GPU (on different streams, or from different models on the
+ * same GPU) race on it; calls in stream order on one stream do not. */
+int sf_modulation_noalloc(sf_model* m, const float* t, int B, float* table, void* hip_stream);
+
 /* Test hook: run the network on B rows (cond as in sf_velocity) through the patch
  * embedding and the first `blocks` blocks (0..L) and copy the fp32 residual stream to
  * h: device [rows][N][D]. */

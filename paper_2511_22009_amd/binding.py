@@ -82,6 +82,7 @@ _SIGS = {
     "sf_stream_step": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P]),
     "sf_euler_shift": (_I, [_P, _P, _P, _P, _I, _P, _P, _P]),
     "sf_modulation": (_I, [_P, _P, _I, _P, _P]),
+    "sf_modulation_noalloc": (_I, [_P, _P, _I, _P, _P]),
     "sf_residual": (_I, [_P, _P, _P, _I, _P, _I, _P, _P]),
     "sf_debug_read": (_I, [_P, _I, _P, ctypes.c_size_t, _P]),
     "sf_timing_enable": (_I, [_P, _I, _I]),
@@ -240,6 +241,18 @@ class Model:
             raise ValueError("table: expected contiguous float32 [B, mod_width]")
         _check(load_library().sf_modulation(self._h, _ptr(tt), B, ctypes.c_void_p(out.data_ptr()),
                                             self._stream(stream)), "sf_modulation")
+        return out
+
+    def modulation_noalloc(self, t, out, stream=None):
+        """sf_modulation_noalloc: the table of `modulation`, computed with the library's
+        fixed scratch array (no device allocation); `out` is required."""
+        tt = np.ascontiguousarray(np.asarray(t, dtype=np.float32).reshape(-1))
+        B = tt.shape[0]
+        import torch
+        if out.dtype != torch.float32 or not out.is_contiguous() or out.numel() < B * self.info["mod_width"]:
+            raise ValueError("table: expected contiguous float32 [B, mod_width]")
+        _check(load_library().sf_modulation_noalloc(self._h, _ptr(tt), B, ctypes.c_void_p(out.data_ptr()),
+                                                    self._stream(stream)), "sf_modulation_noalloc")
         return out
 
     def residual(self, x, t, blocks, cond=None, stream=None):

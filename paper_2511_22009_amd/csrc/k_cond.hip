@@ -6,6 +6,8 @@
 //    cost no more than one shared t would.
 //  * K2, patchify + patch embedding + position table.
 //  * context assembly for the cross-attention K/V projection.
+#include <mutex>
+
 #include "sf_device.h"
 
 namespace sf {
@@ -275,6 +277,33 @@ hipError_t launch_ctx_assemble(bool use_bf16, const float* ctx, const float* nul
     launch(ctx_assemble_kernel<float>, dim3(grid), dim3(256), 0, s, ctx, null_ctx,
                        n_cond, rows, per_row, (float*)out);
   return hipGetLastError();
+}
+
+// Scratch of the allocation-free conditioning call: the timestep MLP's hidden layer and
+// SiLU(c), each [kMaxRows][kMaxWidth] fp32 (1 MiB in all). One copy per GPU, allocated
+// with the code object and held until the process ends. Host code never passes the
+// symbol itself to a kernel: it looks up the device address once per device
+// (modulation_scratch) and uses that.
+static __device__ __align__(256) float scratch[2 * kMaxRows * kMaxWidth];
+
+hipError_t modulation_scratch(float** out, size_t* floats) {
+  constexpr int kDevices = 64;
+  static std::mutex mu;
+  static float* addr[kDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return e != hipSuccess ? e : hipErrorInvalidSymbol;
+    addr[dev] = (float*)p;
+  }
+  *out = addr[dev];
+  *floats = sizeof(scratch) / sizeof(float);
+  return hipSuccess;
 }
 
 }  // namespace sf

@@ -60,6 +60,9 @@ struct GemvArgs {
   RowScalars t;         // (x_mode 1)
 };
 hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s);
+// Device address (on the current device) and size in floats of the fixed scratch array
+// of the allocation-free conditioning call; looked up once per device.
+hipError_t modulation_scratch(float** out, size_t* floats);
 
 // ---- K2: patchify + patch embed + position table ---------------------------------
 struct EmbedArgs {

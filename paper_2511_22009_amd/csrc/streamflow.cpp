@@ -99,6 +99,9 @@ struct sf_model {
   std::vector<Block> blk;
   // workspace
   float *hid = nullptr, *svec = nullptr, *table = nullptr, *h = nullptr, *vrows = nullptr;
+  // the fixed scratch array of sf_modulation_noalloc on this model's device
+  float* scratch = nullptr;
+  size_t scratch_floats = 0;
   void *act = nullptr, *q = nullptr, *k = nullptr, *vT = nullptr, *o = nullptr, *f = nullptr;
   void *ctxA = nullptr, *kx = nullptr, *vTx = nullptr;
   int ldv = 0, ldvx = 0;
@@ -347,8 +350,9 @@ int timed(sf_model* m, int kc, hipStream_t s, F&& launch) {
     if (rc_ != SF_OK) return rc_; \
   } while (0)
 
-// Per-sample conditioning: t[k] -> adaLN table row k (width modw).
-int run_modulation(sf_model* m, const float* t, int n, float* table, hipStream_t s) {
+// Per-sample conditioning: t[k] -> adaLN table row k (width modw). hid and svec hold the
+// timestep MLP's hidden layer and SiLU(c) ([n][D] each).
+int run_modulation(sf_model* m, const float* t, int n, float* table, hipStream_t s, float* hid, float* svec) {
   const Header& h = m->hd;
   return timed(m, SF_KC_TEMB, s, [&]() -> hipError_t {
     sf::GemvArgs g{};
@@ -357,7 +361,7 @@ int run_modulation(sf_model* m, const float* t, int n, float* table, hipStream_t
     g.B = n;
     g.K = h.tdim;
     g.R = h.D;
-    g.Y = m->hid;
+    g.Y = hid;
     g.ldy = h.D;
     g.act = 1;
     g.x_mode = 1;
@@ -368,12 +372,12 @@ int run_modulation(sf_model* m, const float* t, int n, float* table, hipStream_t
     sf::GemvArgs g2{};
     g2.W = m->W_t2;
     g2.bias = m->b_t2;
-    g2.X = m->hid;
+    g2.X = hid;
     g2.ldx = h.D;
     g2.B = n;
     g2.K = h.D;
     g2.R = h.D;
-    g2.Y = m->svec;
+    g2.Y = svec;
     g2.ldy = h.D;
     g2.act = 1;  // the adaLN projections read SiLU(c)
     e = sf::launch_gemv(false, g2, s);
@@ -381,7 +385,7 @@ int run_modulation(sf_model* m, const float* t, int n, float* table, hipStream_t
     sf::GemvArgs g3{};
     g3.W = m->W_mod;
     g3.bias = m->b_mod;
-    g3.X = m->svec;
+    g3.X = svec;
     g3.ldx = h.D;
     g3.B = n;
     g3.K = h.D;
@@ -412,7 +416,7 @@ int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows
                 int nblocks, float* head_out, hipStream_t s, bool table_ready = false) {
   const Header& h = m->hd;
   const int D = h.D, N = m->N, M = rows * N;
-  if (!table_ready) SF_TRY(run_modulation(m, t, n_lat, m->table, s));
+  if (!table_ready) SF_TRY(run_modulation(m, t, n_lat, m->table, s, m->hid, m->svec));
   SF_TRY(timed(m, SF_KC_EMBED, s, [&]() {
     sf::EmbedArgs e{x, n_lat, m->W_pe, m->b_pe, m->pos, m->h, rows, (int)h.C, (int)h.H, (int)h.W, (int)h.p, D, N};
     return sf::launch_embed(e, s);
@@ -720,6 +724,13 @@ int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows
     sf_free(m);
     return SF_E_OOM;
   }
+  // set-up of the allocation-free conditioning call: the device address of the fixed
+  // scratch array on this (current) device, looked up once per device
+  if (sf::modulation_scratch(&m->scratch, &m->scratch_floats) != hipSuccess) {
+    (void)hipGetLastError();
+    sf_free(m);
+    return SF_E_HIP;
+  }
   fill_weights(m, (const char*)blob, img);
   if (hipMemcpy(m->wmem, img.data(), m->wbytes, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemset(m->wsmem, 0, m->wsbytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
@@ -817,7 +828,18 @@ int sf_euler_shift(sf_model* m, float* x, const float* v, const float* dt, int B
 int sf_modulation(sf_model* m, const float* t, int B, float* table, void* stream) {
   if (!m) return SF_E_NOTLOADED;
   if (!t || !table || B < 1 || B > m->max_rows || !finite_all(t, B)) return SF_E_INVAL;
-  return run_modulation(m, t, B, table, (hipStream_t)stream);
+  return run_modulation(m, t, B, table, (hipStream_t)stream, m->hid, m->svec);
+}
+
+int sf_modulation_noalloc(sf_model* m, const float* t, int B, float* table, void* stream) {
+  if (!m) return SF_E_NOTLOADED;
+  if (!t || !table || B < 1 || B > SF_MAX_ROWS || !finite_all(t, B)) return SF_E_INVAL;
+  // the two [B][D] intermediates must fit the fixed array (B <= 64 and D <= 2048 for
+  // every loaded model, so this holds; checked all the same)
+  if ((size_t)2 * B * m->hd.D > m->scratch_floats || !m->scratch) return SF_E_INVAL;
+  float* hid = m->scratch;
+  float* svec = m->scratch + (size_t)B * m->hd.D;
+  return run_modulation(m, t, B, table, (hipStream_t)stream, hid, svec);
 }
 
 int sf_residual(sf_model* m, const float* x, const float* t, int B, const sf_cond* cond, int blocks, float* hout,
