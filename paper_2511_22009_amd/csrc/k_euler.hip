@@ -7,8 +7,8 @@
 // x' = x + dt (lambda_t x + eta_t eps - x) / (t^e - t) = A_k x + B_k eps, with A_k and
 // B_k computed once per slot in fp64 at the start of every workgroup.
 //
-// In place without a race: each thread owns four elements of the latent and walks the
-// slots from the oldest to the newest, reading slot k before it writes slot k + 1.
+// In place without a race: each thread owns one element of the latent, reads it from
+// every slot, then writes the slots from the oldest to the newest.
 // Products and sums are rounded separately (contraction into FMA is switched off for
 // these functions), so the result is bit-identical to a plain fp32 x + dt * v.
 #include "sf_device.h"
@@ -44,6 +44,11 @@ __device__ void window_coeffs(const EulerArgs& a, int k, float* A, float* B) {
   *B = (float)(c * eta_t);
 }
 
+// One thread per element: it loads the element of every slot (and both guidance rows)
+// first, then writes the updated values oldest first, so every read of slot k precedes
+// the write of slot k + 1 and all of a thread's loads are in flight together. The
+// latent's elements spread over E / 256 workgroups (64 at 512^2).
+template <int BMAX>
 __global__ __launch_bounds__(256) void euler_shift_kernel(EulerArgs a) {
 #pragma clang fp contract(off)
   __shared__ float coef[2][kMaxRows];
@@ -51,34 +56,42 @@ __global__ __launch_bounds__(256) void euler_shift_kernel(EulerArgs a) {
     if ((int)threadIdx.x < a.B) window_coeffs(a, threadIdx.x, &coef[0][threadIdx.x], &coef[1][threadIdx.x]);
     __syncthreads();
   }
-  const int e4 = blockIdx.x * blockDim.x + threadIdx.x;
-  const int n4 = a.E >> 2;
-  if (e4 >= n4) return;
-  float4* x = (float4*)a.x;
-  const float4* v = (const float4*)a.v;
-  for (int k = a.B - 1; k >= 0; --k) {
-    float4 vk = v[(size_t)k * n4 + e4];
-    if (a.guided) vk = guided(vk, v[(size_t)(a.B + k) * n4 + e4], a.w);
-    const float4 xk = x[(size_t)k * n4 + e4];
-    float4 xn;
-    if (a.windows > 0) {
-      const float A = coef[0][k], B = coef[1][k];
-      xn = make_float4(A * xk.x + B * vk.x, A * xk.y + B * vk.y, A * xk.z + B * vk.z, A * xk.w + B * vk.w);
-    } else {
-      const float d = a.dt.v[k];
-      xn = make_float4(xk.x + d * vk.x, xk.y + d * vk.y, xk.z + d * vk.z, xk.w + d * vk.w);
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= a.E) return;
+  const size_t E = a.E;
+  float xs[BMAX], vs[BMAX];
+#pragma unroll
+  for (int k = 0; k < BMAX; ++k) {
+    if (k < a.B) {
+      xs[k] = a.x[k * E + e];
+      vs[k] = a.v[k * E + e];
+      if (a.guided) {
+        const float vu = a.v[(a.B + k) * E + e];
+        vs[k] = vu + a.w * (vs[k] - vu);
+      }
     }
-    if (k == a.B - 1 && a.x_done)
-      ((float4*)a.x_done)[e4] = xn;
-    else
-      x[(size_t)(k + 1) * n4 + e4] = xn;
   }
-  x[e4] = ((const float4*)a.z_new)[e4];
+  const float z = a.z_new[e];
+#pragma unroll
+  for (int k = BMAX - 1; k >= 0; --k) {
+    if (k >= a.B) continue;
+    const float xn = a.windows > 0 ? coef[0][k] * xs[k] + coef[1][k] * vs[k] : xs[k] + a.dt.v[k] * vs[k];
+    if (k == a.B - 1 && a.x_done)
+      a.x_done[e] = xn;
+    else
+      a.x[(k + 1) * E + e] = xn;
+  }
+  a.x[e] = z;
 }
 
 hipError_t launch_euler_shift(const EulerArgs& a, hipStream_t s) {
-  const int n4 = a.E >> 2;
-  launch(euler_shift_kernel, dim3((n4 + 255) / 256), dim3(256), 0, s, a);
+  const dim3 grid((a.E + 255) / 256);
+  if (a.B <= 4)
+    launch(euler_shift_kernel<4>, grid, dim3(256), 0, s, a);
+  else if (a.B <= 16)
+    launch(euler_shift_kernel<16>, grid, dim3(256), 0, s, a);
+  else
+    launch(euler_shift_kernel<kMaxRows>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

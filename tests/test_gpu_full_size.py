@@ -189,7 +189,7 @@ def _bf16_weights(W_):
 def test_s512_kernels_on_their_own_inputs():
     """Every kernel of block 0 at 512^2 in bf16 (the launch configuration the benchmark
     times: the 128x288 QKV tile with the permuted transposed-v store, head-dim-64
-    attention with directly staged K/V, the 128x384 fc1 tile with GELU, the directly
+    attention with directly staged K/V, the 256x192 fc1 tile with GELU, the directly
     staged 128x96 out-projection and fc2 tiles with the gated residual) against fp64
     arithmetic on exactly the inputs that kernel read, element by element:
     |got - ref| <= rel |ref| + floor rms(ref). rel = 2^-8 is one bf16 rounding of the
