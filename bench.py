@@ -44,12 +44,20 @@ MI355X_HBM_GBS = 8000.0
 # --no-sequential --copy-calibration`, each scaled by what the same counter reads for a
 # plain 256 MiB elementwise copy (FETCH_SIZE x 2.000, WRITE_SIZE x 1.000). An entry holds
 # only for the kernel sources it was measured on (hash below); otherwise traffic is null.
-KERNEL_SOURCES = ("k_gemm.hip", "sf_device.h", "sf_launch.h")
+KERNEL_SOURCES = ("k_gemm.hip", "k_attn.hip", "sf_device.h", "sf_launch.h")
 TRAFFIC = {
-    ("s512", "bf16", "FC2"): {"bytes": 94526902, "sources": "06e72fb95d785882",
+    ("s512", "bf16", "FC2"): {"bytes": 94526502, "sources": "78b1dbc3f88e66e0",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512", "bf16", "FC1"): {"bytes": 56844131, "sources": "06e72fb95d785882",
+    ("s512", "bf16", "FC1"): {"bytes": 59973646, "sources": "78b1dbc3f88e66e0",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
+    ("s512_large", "bf16", "FC2"): {"bytes": 185954085, "sources": "78b1dbc3f88e66e0",
+                                    "profile": "profiles/stream_step_s512_large_bf16.md"},
+    ("s512_large", "bf16", "FC1"): {"bytes": 132518135, "sources": "78b1dbc3f88e66e0",
+                                    "profile": "profiles/stream_step_s512_large_bf16.md"},
+    ("s512_cfg", "bf16", "FC2"): {"bytes": 389477503, "sources": "78b1dbc3f88e66e0",
+                                  "profile": "profiles/stream_step_s512_cfg_bf16.md"},
+    ("s1024", "bf16", "ATTN"): {"bytes": 166791190, "sources": "78b1dbc3f88e66e0",
+                                "profile": "profiles/stream_step_s1024_bf16.md"},
 }
 
 
