@@ -257,22 +257,23 @@ def main():
     # distinct call: the fresh-latent pool has 16 entries, so 16 graphs after warm-up)
     graph = None
     cached_mod = None
+    ctx_reuse = None
     if not args.no_graph:
         gs = torch.cuda.Stream()
 
         def gstep(i):
             m.stream_step(x, t, dt, K, pool[i % pool.shape[0]], done, cond, gs)
 
-        def replay_run():
+        def replay_run(fn=gstep):
             torch.cuda.synchronize()
             for i in range(pool.shape[0] + max(2, args.warmup)):
-                gstep(i)
+                fn(i)
             gmarks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
             torch.cuda.synchronize()
             g0 = time.perf_counter()
             for i in range(args.steps):
                 gmarks[i].record(gs)
-                gstep(i)
+                fn(i)
             gmarks[-1].record(gs)
             torch.cuda.synchronize()
             gel = time.perf_counter() - g0
@@ -292,6 +293,23 @@ def main():
         cached_mod = replay_run()
         cached_mod["skipped_conditioning_calls"] = m.modulation_cache_stats()
         m.modulation_cache(False)
+        # reported separately too: with cross-attention, the replayed steps with the
+        # context entries kept across calls while the contexts move through the queue as
+        # in Alg. 2 (a window sliding down a pool of contexts: each step's slot k holds
+        # the context slot k - 1 held the step before, and slot 0 a new one)
+        if cond is not None:
+            P = pool.shape[0]
+            ctx_pool = torch.from_numpy(W.context(cfg, P + K, seed=W.gen.SEED_IMAGE_BASE + 7)).to(dev)
+
+            def cstep(i):
+                w = (P - 1) - (i % P)
+                m.stream_step(x, t, dt, K, pool[i % P], done, Cond(ctx_pool[w:w + K], cond.null_ctx, cond.guidance), gs)
+
+            m.context_cache(True)
+            ctx_reuse = replay_run(cstep)
+            calls, projected = m.context_cache_stats()
+            ctx_reuse["contexts_projected_per_step"] = projected / max(calls, 1)
+            m.context_cache(False)
         m.graph_enable(False)
 
     # Alg. 2 end to end: M = 100 images through the fill phase and the full queue
@@ -363,6 +381,7 @@ def main():
         "graph_replay": graph,
         "eager": eager,
         "graph_replay_modulation_cached": cached_mod,
+        "graph_replay_context_reuse": ctx_reuse,
         "step_tflops": cfg.flops_per_step() / (head_ms / 1e3) / 1e12,
         "step_frac_of_peak": cfg.flops_per_step() / (head_ms / 1e3) / 1e12 / peak,
         "gemm_tflops": gemm_tflops,

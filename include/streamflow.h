@@ -271,6 +271,28 @@ int sf_modulation_cache(sf_model* m, int enable);
 /* Number of network calls that reused the cached table (skips counted at enqueue). */
 int sf_modulation_cache_stats(const sf_model* m, long* skips);
 
+/* Context reuse for cross-attention (Alg. 2: the conditioning c of each latent stays
+ * with it while it moves through the queue, and ApplyCFG / HandleCFG pair every latent
+ * with the one unconditional context). The keys and values of a context depend on the
+ * context and the weights only. Every network call keeps them per context ENTRY for all
+ * blocks at once: the B conditional rows use the entries of their own contexts and all
+ * unconditional rows share the entry of null_ctx (computed once per call, not per row).
+ * While enabled, entries also outlive the call: each slot's context is compared, bitwise
+ * and on the GPU, with the context of the entry that slot used in the previous call and
+ * with that of the entry of the slot before it (where the shift of sf_stream_step moved
+ * it), likewise the null context; an equal one is reused and only the others are
+ * projected. Results are bit-identical to calls without reuse. The entries live in the
+ * model's workspace and are updated in stream order, so calls that use the cache must
+ * run in order on one stream. Off by default. Enabling or disabling forgets every entry
+ * and waits for the device; a failed call forgets them too. A no-op (SF_OK) for networks
+ * without cross-attention. Returns SF_E_NOTLOADED for a null model, SF_E_HIP on a HIP
+ * failure. */
+int sf_context_cache(sf_model* m, int enable);
+/* Calls that went through the entry lookup while enabled, and the context entries they
+ * projected (the rest were reused). Waits for the device. Zero for networks without
+ * cross-attention. */
+int sf_context_cache_stats(const sf_model* m, long* calls, long* projected);
+
 /* Test and bench hook: while enabled, every launch of kernel class `kc` is timed by a
  * pair of HIP events. For a class that is one kernel the events are attached to that
  * kernel's dispatch (its own start and end); SF_KC_TEMB and SF_KC_CROSS, which launch

@@ -94,6 +94,8 @@ _SIGS = {
     "sf_graph_stats": (_I, [_P, ctypes.POINTER(_I), ctypes.POINTER(ctypes.c_long)]),
     "sf_modulation_cache": (_I, [_P, _I]),
     "sf_modulation_cache_stats": (_I, [_P, ctypes.POINTER(ctypes.c_long)]),
+    "sf_context_cache": (_I, [_P, _I]),
+    "sf_context_cache_stats": (_I, [_P, ctypes.POINTER(ctypes.c_long), ctypes.POINTER(ctypes.c_long)]),
 }
 
 
@@ -323,6 +325,18 @@ class Model:
         skips = ctypes.c_long()
         _check(load_library().sf_modulation_cache_stats(self._h, ctypes.byref(skips)), "sf_modulation_cache_stats")
         return skips.value
+
+    def context_cache(self, on=True):
+        """Keep the cross-attention context entries across calls, reusing an entry whose
+        context is bitwise unchanged (see sf_context_cache). Waits for the device."""
+        _check(load_library().sf_context_cache(self._h, 1 if on else 0), "sf_context_cache")
+
+    def context_cache_stats(self):
+        """(calls through the entry lookup, context entries projected by them)."""
+        calls, projected = ctypes.c_long(0), ctypes.c_long(0)
+        _check(load_library().sf_context_cache_stats(self._h, ctypes.byref(calls), ctypes.byref(projected)),
+               "sf_context_cache_stats")
+        return calls.value, projected.value
 
     def timing_enable(self, kc, on=True):
         _check(load_library().sf_timing_enable(self._h, int(kc), 1 if on else 0), "sf_timing_enable")

@@ -69,9 +69,10 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const int head = rh % a.heads, r = rh / a.heads;
   const int dh = a.dh;
   const size_t bh = (size_t)r * a.heads + head;
+  const size_t kr = a.kv_map ? (size_t)a.kv_map[r] : (size_t)r;  // the row whose keys and values r reads
   const bf16* Q = (const bf16*)a.q + bh * a.Nq * dh;
-  const bf16* Kg = (const bf16*)a.k + bh * a.Nk * dh;
-  const bf16* Vt = (const bf16*)a.vT + bh * dh * a.ldv;
+  const bf16* Kg = (const bf16*)a.k + kr * a.k_rs + (size_t)head * a.Nk * dh;
+  const bf16* Vt = (const bf16*)a.vT + kr * a.v_rs + (size_t)head * dh * a.ldv;
   const int qi = qblk * kQB + qg * 32 + l32;
 
   // zero the tile buffers once: padding columns (dh..KLD) and rows (dh..VROWS) are
@@ -301,9 +302,10 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   const int rh = logical / nqb;
   const int head = rh % a.heads, r = rh / a.heads;
   const size_t bh = (size_t)r * a.heads + head;
+  const size_t kr = a.kv_map ? (size_t)a.kv_map[r] : (size_t)r;  // the row whose keys and values r reads
   const bf16* Q = (const bf16*)a.q + bh * a.Nq * DH;
-  const bf16* Kg = (const bf16*)a.k + bh * a.Nk * DH;
-  const bf16* Vt = (const bf16*)a.vT + bh * DH * a.ldv;
+  const bf16* Kg = (const bf16*)a.k + kr * a.k_rs + (size_t)head * a.Nk * DH;
+  const bf16* Vt = (const bf16*)a.vT + kr * a.v_rs + (size_t)head * DH * a.ldv;
   const int qi = qblk * kQB + qg * 32 + l32;
 
   bf16x8 qf[DHC];
@@ -476,9 +478,10 @@ __global__ __launch_bounds__(128) void attn_f32_kernel(AttnArgs a) {
   const int head = blockIdx.y, r = blockIdx.z;
   const int dh = a.dh;
   const size_t bh = (size_t)r * a.heads + head;
+  const size_t kr = a.kv_map ? (size_t)a.kv_map[r] : (size_t)r;  // the row whose keys and values r reads
   const float* Q = (const float*)a.q + bh * a.Nq * dh;
-  const float* Kg = (const float*)a.k + bh * a.Nk * dh;
-  const float* Vt = (const float*)a.vT + bh * dh * a.ldv;
+  const float* Kg = (const float*)a.k + kr * a.k_rs + (size_t)head * a.Nk * dh;
+  const float* Vt = (const float*)a.vT + kr * a.v_rs + (size_t)head * dh * a.ldv;
   const int qi = blockIdx.x * blockDim.x + threadIdx.x;
   float q[DHMAX], o[DHMAX];
 #pragma unroll
@@ -531,7 +534,10 @@ static void launch_bf16_inst(const AttnArgs& a, hipStream_t s) {
     launch((attn_bf16_kernel<DHC, DB, false>), grid, dim3(256), 0, s, a);
 }
 
-hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attention(bool use_bf16, const AttnArgs& args, hipStream_t s) {
+  AttnArgs a = args;
+  if (!a.k_rs) a.k_rs = (size_t)a.heads * a.Nk * a.dh;
+  if (!a.v_rs) a.v_rs = (size_t)a.heads * a.dh * a.ldv;
   if (!attention_supports(a.dh)) return hipErrorInvalidValue;
   // the bf16 kernels read transposed v in the permuted key layout only, with rows of
   // whole 64-key steps; the fp32 kernel reads the plain layout

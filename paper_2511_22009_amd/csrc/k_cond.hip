@@ -5,7 +5,8 @@
 //    read from HBM serves every sample), so the heterogeneous timesteps of Sec. 3.2
 //    cost no more than one shared t would.
 //  * K2, patchify + patch embedding + position table.
-//  * context assembly for the cross-attention K/V projection.
+//  * the context entries of the cross-attention keys and values (assembly, and the
+//    bitwise lookup that reuses an entry while its context stays in the queue).
 #include <mutex>
 
 #include "sf_device.h"
@@ -252,30 +253,156 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- context entries
+// Network row r of a call with B slots: r < B conditional (entry of slot r), r >= B
+// unconditional (the null-context entry, context row B).
+__device__ __forceinline__ void write_kv_map(CtxState* st, int B, int guided, const int* ent) {
+  const int rows = guided ? 2 * B : B;
+  for (int r = threadIdx.x; r < rows; r += blockDim.x) st->kv_map[r] = ent[r < B ? r : B];
+}
+
+// Without reuse: entry j is context row j (j < B: ctx[j], j == B: the null context).
 template <typename T>
-__global__ __launch_bounds__(256) void ctx_assemble_kernel(const float* ctx, const float* null_ctx,
-                                                           int n_cond, int rows, int per_row, T* out) {
-  const size_t total = (size_t)rows * per_row;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (size_t)gridDim.x * blockDim.x) {
-    const int r = (int)(i / per_row);
-    const size_t e = i - (size_t)r * per_row;
-    const float v = r < n_cond ? ctx[(size_t)r * per_row + e] : null_ctx[e];
-    out[i] = from_f32<T>(v);
+__global__ __launch_bounds__(256) void ctx_prepare_kernel(CtxArgs a) {
+  if (blockIdx.x == 0) {
+    __shared__ int ent[kMaxRows + 1];
+    for (int j = threadIdx.x; j <= a.B; j += blockDim.x) ent[j] = j;
+    __syncthreads();
+    write_kv_map(a.st, a.B, a.guided, ent);
+  }
+  const size_t total = (size_t)(a.B + a.guided) * a.per_row;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const int j = (int)(i / a.per_row);
+    const size_t e = i - (size_t)j * a.per_row;
+    const float v = j < a.B ? a.ctx[i] : a.null_ctx[e];
+    ((T*)a.ctxA)[i] = from_f32<T>(v);
   }
 }
 
-hipError_t launch_ctx_assemble(bool use_bf16, const float* ctx, const float* null_ctx, int n_cond,
-                               int rows, int ctx_len, int ctx_dim, void* out, hipStream_t s) {
-  const int per_row = ctx_len * ctx_dim;
-  int grid = (int)(((size_t)rows * per_row + 255) / 256);
+// The two entries context row j may reuse: c0 the entry its slot held in the previous
+// call, c1 the entry of the slot before it (Alg. 2's shift moves a latent and its
+// context one slot on per step); the null row has only the previous null entry.
+__device__ __forceinline__ void ctx_candidates(const CtxState* st, int B, int j, int& c0, int& c1) {
+  if (j == B) {
+    c0 = st->prev_null - 1;
+    c1 = -1;
+  } else {
+    c0 = j < st->prev_B ? st->prev_slot[j] : -1;
+    c1 = (j >= 1 && j - 1 < st->prev_B) ? st->prev_slot[j - 1] : -1;
+  }
+}
+
+constexpr int kCtxChunk = 256 * 8;  // floats compared / copied per workgroup
+
+// grid (context rows, chunks): bitwise comparison of each context row with the stored
+// context of its candidate entries; a difference anywhere sets the candidate's bit.
+__global__ __launch_bounds__(256) void ctx_compare_kernel(CtxArgs a) {
+  const int j = blockIdx.x;
+  int c[2];
+  ctx_candidates(a.st, a.B, j, c[0], c[1]);
+  const float* row = j < a.B ? a.ctx + (size_t)j * a.per_row : a.null_ctx;
+  const int i0 = blockIdx.y * kCtxChunk;
+  int bits = 0;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    if (c[q] < 0) continue;
+    const float* kp = a.keep + (size_t)c[q] * a.per_row;
+    bool diff = false;
+    for (int i = i0 + threadIdx.x; i < i0 + kCtxChunk && i < a.per_row; i += 256)
+      diff |= __float_as_uint(row[i]) != __float_as_uint(kp[i]);
+    if (__any(diff)) bits |= 1 << q;
+  }
+  if ((threadIdx.x & 63) == 0 && bits) atomicOr(&a.st->flags[j], bits);
+}
+
+// One thread: picks each context row's entry (a matching candidate, else an entry no
+// row of this call uses), marks the new ones live, writes kv_map, and keeps this call's
+// slot entries as the next call's candidates.
+__global__ __launch_bounds__(64) void ctx_assign_kernel(CtxArgs a) {
+  if (threadIdx.x != 0) return;
+  CtxState* st = a.st;
+  const int rc = a.B + a.guided;
+  int ent[kMaxRows + 1];
+  bool taken[kMaxRows + 1];
+  for (int e = 0; e < a.n_entries; ++e) {
+    taken[e] = false;
+    st->live[e] = 0;
+    st->src[e] = -1;
+  }
+  for (int j = 0; j < rc; ++j) {
+    int c0, c1;
+    ctx_candidates(st, a.B, j, c0, c1);
+    const int fl = st->flags[j];
+    int e = -1;
+    if (c0 >= 0 && !(fl & 1)) e = c0;
+    else if (c1 >= 0 && !(fl & 2)) e = c1;
+    ent[j] = e;
+    if (e >= 0) taken[e] = true;
+  }
+  int next = 0, fresh = 0;
+  for (int j = 0; j < rc; ++j) {
+    if (ent[j] >= 0) continue;
+    while (taken[next]) ++next;  // rc <= n_entries, so a free entry exists
+    ent[j] = next;
+    taken[next] = true;
+    st->live[next] = 1;
+    st->src[next] = j;
+    ++fresh;
+  }
+  const int rows = a.guided ? 2 * a.B : a.B;
+  for (int r = 0; r < rows; ++r) st->kv_map[r] = ent[r < a.B ? r : a.B];
+  for (int j = 0; j < a.B; ++j) st->prev_slot[j] = ent[j];
+  st->prev_B = a.B;
+  st->prev_null = a.guided ? ent[a.B] + 1 : 0;
+  for (int j = 0; j <= kMaxRows; ++j) st->flags[j] = 0;
+  st->calls += 1;
+  st->computed += (unsigned long long)fresh;
+}
+
+// grid (entries, chunks): a live entry takes its context row (kept in fp32 for later
+// comparisons, and in the compute type as the K/V GEMM operand).
+template <typename T>
+__global__ __launch_bounds__(256) void ctx_fill_kernel(CtxArgs a) {
+  const int e = blockIdx.x;
+  if (!a.st->live[e]) return;
+  const int j = a.st->src[e];
+  const float* row = j < a.B ? a.ctx + (size_t)j * a.per_row : a.null_ctx;
+  const int i0 = blockIdx.y * kCtxChunk;
+  for (int i = i0 + threadIdx.x; i < i0 + kCtxChunk && i < a.per_row; i += 256) {
+    const float v = row[i];
+    a.keep[(size_t)e * a.per_row + i] = v;
+    ((T*)a.ctxA)[(size_t)e * a.per_row + i] = from_f32<T>(v);
+  }
+}
+
+__global__ __launch_bounds__(64) void ctx_reset_kernel(CtxState* st) {
+  int* p = (int*)st;
+  for (int i = threadIdx.x; i < (int)(sizeof(CtxState) / sizeof(int)); i += 64) p[i] = 0;
+}
+
+hipError_t launch_ctx_prepare(bool use_bf16, const CtxArgs& a, hipStream_t s) {
+  int grid = (int)(((size_t)(a.B + a.guided) * a.per_row + 255) / 256);
   if (grid > 4096) grid = 4096;
   if (use_bf16)
-    launch(ctx_assemble_kernel<bf16>, dim3(grid), dim3(256), 0, s, ctx, null_ctx,
-                       n_cond, rows, per_row, (bf16*)out);
+    launch(ctx_prepare_kernel<bf16>, dim3(grid), dim3(256), 0, s, a);
   else
-    launch(ctx_assemble_kernel<float>, dim3(grid), dim3(256), 0, s, ctx, null_ctx,
-                       n_cond, rows, per_row, (float*)out);
+    launch(ctx_prepare_kernel<float>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ctx_lookup(bool use_bf16, const CtxArgs& a, hipStream_t s) {
+  const int chunks = (a.per_row + kCtxChunk - 1) / kCtxChunk;
+  launch(ctx_compare_kernel, dim3(a.B + a.guided, chunks), dim3(256), 0, s, a);
+  launch(ctx_assign_kernel, dim3(1), dim3(64), 0, s, a);
+  if (use_bf16)
+    launch(ctx_fill_kernel<bf16>, dim3(a.n_entries, chunks), dim3(256), 0, s, a);
+  else
+    launch(ctx_fill_kernel<float>, dim3(a.n_entries, chunks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ctx_reset(CtxState* st, hipStream_t s) {
+  launch(ctx_reset_kernel, dim3(1), dim3(64), 0, s, st);
   return hipGetLastError();
 }
 

@@ -5,7 +5,9 @@
 //   RES_GATE h += gate[sample][n] * (acc + bias), the gate row picked by the token's
 //            sample, i.e. each sample's own timestep (adaLN gate);
 //   GELU     out = GELU_tanh(acc + bias);
-//   RES      h += acc + bias.
+//   RES      h += acc + bias;
+//   KVX      + bias, the cross-attention keys and transposed values of every block at
+//            once (one context entry per network row).
 //
 // bf16 path: v_mfma_f32_32x32x16_bf16 on BM x BN x BK workgroup tiles (BK 64 or 128;
 // table at the end), each wavefront owning a 64x64, 64x96 or 32x96 sub-tile, optionally with
@@ -22,18 +24,46 @@
 
 namespace sf {
 
+// Destination of a projection column in part `part` (= n / D) of network row r: QKV
+// part which_base + part (0 q, 1 k, 2 v) of row r; KVX the key (even part) or value of
+// block part / 2, stored as row r * L + block of the [rows][heads][...] layouts.
+template <EpiKind KIND>
+__device__ __forceinline__ void qkv_dest(const GemmArgs& a, int part, int r, int& which, int& rr) {
+  if constexpr (KIND == EPI_KVX) {
+    which = 1 + (part & 1);
+    rr = r * a.kv_blocks + (part >> 1);
+  } else {
+    which = a.which_base + part;
+    rr = r;
+  }
+}
+
+// True when the tile of rows m0 .. m0 + BM - 1 holds a row whose entry is live (or no
+// liveness is given): the caller skips the whole tile otherwise.
+template <EpiKind KIND, int BM>
+__device__ __forceinline__ bool tile_live(const GemmArgs& a, int m0) {
+  if constexpr (KIND != EPI_KVX) return true;
+  if (!a.row_live) return true;
+  const int r0 = (int)fdiv((uint32_t)m0, a.div_ntok);
+  const int r1 = (int)fdiv((uint32_t)(min(m0 + BM, a.M) - 1), a.div_ntok);
+  for (int r = r0; r <= r1; ++r)
+    if (a.row_live[r]) return true;
+  return false;
+}
+
 template <EpiKind KIND, typename OT>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, int m, int n, float acc) {
   const float val = acc + a.bias[n];
-  if constexpr (KIND == EPI_QKV) {
+  if constexpr (KIND == EPI_QKV || KIND == EPI_KVX) {
     const int part = (int)fdiv((uint32_t)n, a.div_D);
     const int rem = n - part * a.D;
     const int head = (int)fdiv((uint32_t)rem, a.div_dh);
     const int d = rem - head * a.dh;
-    const int r = (int)fdiv((uint32_t)m, a.div_ntok);
-    const int tok = m - r * a.ntok;
+    const int r0 = (int)fdiv((uint32_t)m, a.div_ntok);
+    const int tok = m - r0 * a.ntok;
+    int which, r;
+    qkv_dest<KIND>(a, part, r0, which, r);
     const size_t bh = (size_t)r * a.heads + head;
-    const int which = a.which_base + part;
     // Destination picked with selects, not a three-way branch: this compiler lowered
     // the divergent if / else-if / else form to code that stored the v part through
     // the k pointer.
@@ -125,7 +155,7 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const float* 
 template <EpiKind KIND, int RP, int BN, int NT>
 struct ResItems {
   static_assert(KIND == EPI_RES || KIND == EPI_RES_GATE || KIND == EPI_RES_GATE_MLP || KIND == EPI_GELU ||
-                    KIND == EPI_QKV,
+                    KIND == EPI_QKV || KIND == EPI_KVX,
                 "epilogue kind");
   static constexpr bool kGate = KIND == EPI_RES_GATE || KIND == EPI_RES_GATE_MLP;
   static constexpr int C4 = BN / 4;
@@ -237,22 +267,23 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
         *(u32x4*)((bf16*)a.out + (size_t)m * a.ldo + n) = val[u];
       } else {
         const int part = (int)fdiv((uint32_t)n, a.div_D);
-        const int which = a.which_base + part;
         const int rem = n - part * a.D;
         const int head = (int)fdiv((uint32_t)rem, a.div_dh);
         const int d = rem - head * a.dh;
-        const int r = (int)fdiv((uint32_t)m, a.div_ntok);
-        const int tok = m - r * a.ntok;
+        const int r0 = (int)fdiv((uint32_t)m, a.div_ntok);
+        const int tok = m - r0 * a.ntok;
+        int which, r;
+        qkv_dest<KIND>(a, part, r0, which, r);
         bf16* base = (bf16*)(which == 0 ? a.q : a.k);
         if (which < 2) *(u32x4*)(base + (((size_t)r * a.heads + head) * a.ntok + tok) * a.dh + d) = val[u];
       }
     }
   }
-  if constexpr (KIND == EPI_QKV) {
+  if constexpr (KIND == EPI_QKV || KIND == EPI_KVX) {
     // transposed v, skipped unless the tile reaches the v columns. Plain layout: item =
     // (column, 8 consecutive rows), one 16-byte store. Items that end a network row early
     // or start unaligned go element-wise.
-    if (a.which_base + (int)fdiv((uint32_t)min(n0 + BN, a.N) - 1, a.div_D) < 2) return;
+    if (KIND == EPI_QKV && a.which_base + (int)fdiv((uint32_t)min(n0 + BN, a.N) - 1, a.div_D) < 2) return;
     auto v_items = [&]() {
       constexpr int RG = 8;
       constexpr int VT = BM / RG * BN;
@@ -263,12 +294,14 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
         const int n = n0 + col, m = m0 + rb * RG;
         if ((VT % NT != 0 && c >= VT) || n >= a.N || m >= a.M) continue;
         const int part = (int)fdiv((uint32_t)n, a.div_D);
-        if (a.which_base + part < 2) continue;
         const int rem = n - part * a.D;
         const int head = (int)fdiv((uint32_t)rem, a.div_dh);
         const int d = rem - head * a.dh;
-        const int r = (int)fdiv((uint32_t)m, a.div_ntok);
-        const int tok = m - r * a.ntok;
+        const int r0 = (int)fdiv((uint32_t)m, a.div_ntok);
+        const int tok = m - r0 * a.ntok;
+        int which, r;
+        qkv_dest<KIND>(a, part, r0, which, r);
+        if (which < 2) continue;
         const bf16* cp = Cs + (rb * RG) * CPB + col;
         bf16* vt = (bf16*)a.vT + (((size_t)r * a.heads + head) * a.dh + d) * a.ldv;
         if (tok + RG <= a.ntok && m + RG <= a.M && (tok & (RG - 1)) == 0) {
@@ -279,8 +312,10 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
         } else {
           for (int e = 0; e < RG && m + e < a.M; ++e) {
             const int me = m + e;
-            const int re = (int)fdiv((uint32_t)me, a.div_ntok);
-            const int te = me - re * a.ntok;
+            const int re0 = (int)fdiv((uint32_t)me, a.div_ntok);
+            const int te = me - re0 * a.ntok;
+            int we, re;
+            qkv_dest<KIND>(a, part, re0, we, re);
             ((bf16*)a.vT)[(((size_t)re * a.heads + head) * a.dh + d) * a.ldv + te] =
                 cp[e * CPB];
           }
@@ -300,12 +335,14 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
         const int n = n0 + cg * 8, m = m0 + rb * 16;
         if ((VT % NT != 0 && c >= VT) || n >= a.N || m >= a.M) continue;
         const int part = (int)fdiv((uint32_t)n, a.div_D);
-        if (a.which_base + part < 2) continue;
         const int rem = n - part * a.D;
         const int head = (int)fdiv((uint32_t)rem, a.div_dh);
         const int d0 = rem - head * a.dh;  // the 8 columns are dims d0.. of one head (dh % 8 == 0)
-        const int r = (int)fdiv((uint32_t)m, a.div_ntok);
-        const int tok = m - r * a.ntok;
+        const int r0 = (int)fdiv((uint32_t)m, a.div_ntok);
+        const int tok = m - r0 * a.ntok;
+        int which, r;
+        qkv_dest<KIND>(a, part, r0, which, r);
+        if (which < 2) continue;
         if (tok + 16 <= a.ntok && m + 16 <= a.M && (tok & 15) == 0 && n + 8 <= a.N) {
           u32x4 rows[16];
 #pragma unroll
@@ -323,8 +360,10 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
         } else {
           for (int e = 0; e < 16 && m + e < a.M; ++e) {
             const int me = m + e;
-            const int re = (int)fdiv((uint32_t)me, a.div_ntok);
-            const int te = me - re * a.ntok;
+            const int re0 = (int)fdiv((uint32_t)me, a.div_ntok);
+            const int te = me - re0 * a.ntok;
+            int we, re;
+            qkv_dest<KIND>(a, part, re0, we, re);
             for (int j = 0; j < 8 && n + j < a.N; ++j)
               ((bf16*)a.vT)[(((size_t)re * a.heads + head) * a.dh + d0 + j) * a.ldv + vt_pos(te)] =
                   Cs[(rb * 16 + e) * CPB + cg * 8 + j];
@@ -411,8 +450,9 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
   int mt, nt;
   tile_coords((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
+  if (!tile_live<KIND, BM>(a, m0)) return;  // uniform across the workgroup
   // the tile's bias columns go to LDS now, so the epilogue does not wait on them
-  constexpr bool kBf16Out = KIND == EPI_GELU || KIND == EPI_QKV;
+  constexpr bool kBf16Out = KIND == EPI_GELU || KIND == EPI_QKV || KIND == EPI_KVX;
   __shared__ __attribute__((aligned(16))) float bias_s[kBf16Out ? BN : 4];
   if constexpr (kBf16Out) {
     for (int c = tid; c < BN / 4; c += NT) {
@@ -619,7 +659,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   constexpr int KS = BK / 16 / KSPLIT;  // MFMA K steps per slice and wavefront
   static_assert(KS * 16 * KSPLIT == BK, "K split must divide the K slice");
   static_assert(STAGES == 3 || STAGES == 4, "three or four stages");
-  constexpr bool kBf16Out = KIND == EPI_GELU || KIND == EPI_QKV;
+  constexpr bool kBf16Out = KIND == EPI_GELU || KIND == EPI_QKV || KIND == EPI_KVX;
   // each stage buffer also holds, after the main loop, one row block of the K-split
   // partial sums, one half of the fp32 output tile, or the whole bf16 output tile
   constexpr int CP = BN + 4;
@@ -659,6 +699,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   int mt, nt;
   tile_coords((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
+  if (!tile_live<KIND, BM>(a, m0)) return;  // uniform across the workgroup
   __shared__ __attribute__((aligned(16))) float bias_s[kBf16Out ? BN : 4];
   if constexpr (kBf16Out) {
     for (int c = tid; c < BN / 4; c += NT) {
@@ -864,6 +905,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   const int tid = threadIdx.x;
   const int tx = tid & 15, ty = tid >> 4;
   const int m0 = blockIdx.y * kFT, n0 = blockIdx.x * kFT;
+  if (!tile_live<KIND, kFT>(a, m0)) return;
   const float* A = (const float*)a.A;
   const float* B = (const float*)a.B;
   float acc[4][4] = {};
@@ -987,6 +1029,7 @@ hipError_t launch_gemm_tile(bool use_bf16, int tile, EpiKind kind, const GemmArg
     case EPI_GELU: return launch_kind<EPI_GELU>(use_bf16, tile, a, s);
     case EPI_RES: return launch_kind<EPI_RES>(use_bf16, tile, a, s);
     case EPI_RES_GATE_MLP: return launch_kind<EPI_RES_GATE_MLP>(use_bf16, tile, a, s);
+    case EPI_KVX: return launch_kind<EPI_KVX>(use_bf16, tile, a, s);
   }
   return hipErrorInvalidValue;
 }

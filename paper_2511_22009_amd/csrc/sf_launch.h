@@ -76,10 +76,44 @@ struct EmbedArgs {
 };
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 
-// Build the context matrix of the cross-attention K/V projection:
-// out[r][l][c] = (r < n_cond ? ctx[r] : null_ctx)[l][c], converted to the compute type.
-hipError_t launch_ctx_assemble(bool use_bf16, const float* ctx, const float* null_ctx, int n_cond,
-                               int rows, int ctx_len, int ctx_dim, void* out, hipStream_t s);
+// ---- context entries of the cross-attention K/V ------------------------------------
+// The keys and values of a context depend on the context and the weights only, so they
+// are computed per ENTRY (one context) for every block at once, and each network row
+// reads the entry of its context through kv_map: the B conditional rows their own
+// contexts, every unconditional row the one null-context entry. Device-side state of
+// the entries (one block of ints in the workspace):
+struct CtxState {
+  int kv_map[kMaxRows];        // network row -> entry
+  int prev_slot[kMaxRows];     // entry of each conditional slot in the previous call
+  int flags[kMaxRows + 1];     // per context row of a call: bit 0 / bit 1 set when it
+                               // differs from the entry of the same / the previous slot
+  int live[kMaxRows + 1];      // entries whose keys and values this call computes
+  int src[kMaxRows + 1];       // the context row that fills a live entry
+  int prev_B;                  // conditional slots of the previous call (0: none known)
+  int prev_null;               // entry of the null context in the previous call + 1
+  unsigned long long calls;    // calls through the entry lookup
+  unsigned long long computed; // entries computed by them
+};
+struct CtxArgs {
+  const float* ctx;       // [B][ctx_len][ctx_dim]
+  const float* null_ctx;  // [ctx_len][ctx_dim] (guided) or nullptr
+  int B, guided;          // context rows of the call: B, plus one null row if guided
+  int per_row;            // ctx_len * ctx_dim
+  int n_entries;          // entries held (max_rows + 1)
+  float* keep;            // [n_entries][per_row]: the context each entry was computed from
+  void* ctxA;             // [n_entries][per_row]: the same in the compute type (GEMM operand)
+  CtxState* st;
+};
+// Without reuse: entries 0..B-1 take the conditional contexts, entry B the null
+// context; kv_map accordingly. One kernel.
+hipError_t launch_ctx_prepare(bool use_bf16, const CtxArgs& a, hipStream_t s);
+// With reuse: each context row is compared bitwise with the entry its slot held in the
+// previous call and with the entry of the previous slot (where Alg. 2's shift moved it);
+// a row equal to either reuses that entry, the others take entries no row of this call
+// uses, which are marked live and filled. Three kernels (compare, assign, fill).
+hipError_t launch_ctx_lookup(bool use_bf16, const CtxArgs& a, hipStream_t s);
+// Forgets every entry (no row of the next call can reuse one).
+hipError_t launch_ctx_reset(CtxState* st, hipStream_t s);
 
 // ---- K5: LayerNorm (+ per-sample adaLN modulate) ---------------------------------
 struct LnArgs {
@@ -113,8 +147,10 @@ enum EpiKind {
   EPI_RES_GATE = 1,  // h += gate[slot][n] * (acc + bias)
   EPI_GELU = 2,      // out = GELU_tanh(acc + bias)
   EPI_RES = 3,       // h += acc + bias
-  EPI_RES_GATE_MLP = 4  // EPI_RES_GATE for the MLP down-projection (a separate kernel
+  EPI_RES_GATE_MLP = 4, // EPI_RES_GATE for the MLP down-projection (a separate kernel
                         // symbol, so profiles tell it from the attention projection)
+  EPI_KVX = 5           // + bias, the context keys / transposed values of every block:
+                        // column n is block (n / D) / 2, key if (n / D) even else value
 };
 struct GemmArgs {
   const void* A;
@@ -130,6 +166,11 @@ struct GemmArgs {
   void* vT;             // [rows][heads][dh][ldv]; token t at column t, or at vt_pos(t) if vperm
   int heads, dh, D, ntok, ldv, which_base, vperm;
   FastDiv div_ntok, div_D, div_dh;
+  // EPI_KVX: number of blocks L; the keys of block b for network row r land at row
+  // r * L + b of q/k's [rows][heads][ntok][dh] layout (likewise vT)
+  int kv_blocks;
+  // optional (EPI_KVX): a tile whose rows m all have row_live[m / ntok] == 0 is skipped
+  const int* row_live;
   // EPI_RES_GATE / EPI_RES
   float* h;
   int ldh;
@@ -161,6 +202,11 @@ struct AttnArgs {
   int rows, heads, Nq, Nk, dh, ldv, D;
   float scale;          // 1 / sqrt(dh)
   int vperm;
+  // optional: row r reads the keys and values of row kv_map[r] (nullptr: row r), whose
+  // k starts k_rs elements after the previous row's and vT v_rs after (0: heads*Nk*dh
+  // and heads*dh*ldv, the packed layout)
+  const int* kv_map;
+  size_t k_rs, v_rs;
 };
 hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s);
 bool attention_supports(int dh);

@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstddef>
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
@@ -103,7 +104,17 @@ struct sf_model {
   float* scratch = nullptr;
   size_t scratch_floats = 0;
   void *act = nullptr, *q = nullptr, *k = nullptr, *vT = nullptr, *o = nullptr, *f = nullptr;
+  // cross-attention context entries: n_entries contexts (fp32 copy and GEMM operand),
+  // their keys [n_entries][L][heads][ctx_len][dh] and transposed values
+  // [n_entries][L][heads][dh][ldvx] for every block, and the entries' device state
   void *ctxA = nullptr, *kx = nullptr, *vTx = nullptr;
+  float* ctx_keep = nullptr;
+  sf::CtxState* ctx_st = nullptr;
+  int n_entries = 0;
+  bool ctx_cache_on = false;
+  // every block's context K/V projection, contiguous: [L][2D][ctx_dim] and [L][2D]
+  void* W_kvx = nullptr;
+  float* b_kvx = nullptr;
   int ldv = 0, ldvx = 0;
   int vperm = 0;  // transposed v in the permuted key layout (vt_pos): bf16 mode
   Timing timing[SF_KC_COUNT];
@@ -179,7 +190,10 @@ int check_capacity(const Header& h, int max_rows, size_t es) {
   const uint64_t limit = es == 2 ? (uint64_t)sf::kOffOOBHost : (1ull << 31);
   const uint64_t unit = es == 2 ? es : 1;  // bytes (bf16) or elements (fp32)
   if (R * N * widest * unit >= limit) return SF_E_UNSUPPORTED;
-  if (h.has_cross && R * h.ctx_len * (uint64_t)(h.ctx_dim > h.D ? h.ctx_dim : h.D) * unit >= limit)
+  // cross-attention: the context entries (max_rows + 1) and every block's K/V weights,
+  // the operands of one GEMM
+  if (h.has_cross && ((R + 1) * h.ctx_len * (uint64_t)(h.ctx_dim > h.D ? h.ctx_dim : h.D) * unit >= limit ||
+                      (uint64_t)h.L * 2 * h.D * h.ctx_dim * unit >= limit))
     return SF_E_UNSUPPORTED;
   return SF_OK;
 }
@@ -206,7 +220,12 @@ void carve_weights(sf_model* m, Carver& cv) {
   m->W_mod = cv.take<char>((size_t)m->modw * D, m->es);
   m->b_mod = cv.take<float>(m->modw);
   m->blk.resize(h.L);
-  for (auto& b : m->blk) {
+  if (h.has_cross) {
+    m->W_kvx = cv.take<char>((size_t)h.L * 2 * D * h.ctx_dim, m->es);
+    m->b_kvx = cv.take<float>((size_t)h.L * 2 * D);
+  }
+  for (uint32_t l = 0; l < h.L; ++l) {
+    Block& b = m->blk[l];
     b.W_qkv = cv.take<char>(3 * D * D, m->es);
     b.b_qkv = cv.take<float>(3 * D);
     b.W_o = cv.take<char>(D * D, m->es);
@@ -214,8 +233,8 @@ void carve_weights(sf_model* m, Carver& cv) {
     if (h.has_cross) {
       b.W_qx = cv.take<char>(D * D, m->es);
       b.b_qx = cv.take<float>(D);
-      b.W_kvx = cv.take<char>(2 * D * h.ctx_dim, m->es);
-      b.b_kvx = cv.take<float>(2 * D);
+      b.W_kvx = m->W_kvx ? (char*)m->W_kvx + (size_t)l * 2 * D * h.ctx_dim * m->es : nullptr;
+      b.b_kvx = m->b_kvx ? m->b_kvx + (size_t)l * 2 * D : nullptr;
       b.W_ox = cv.take<char>(D * D, m->es);
       b.b_ox = cv.take<float>(D);
     } else {
@@ -246,9 +265,12 @@ void carve_workspace(sf_model* m, Carver& cv) {
   m->o = cv.take<char>(M * D, m->es);
   m->f = cv.take<char>(M * h.mlp, m->es);
   if (h.has_cross) {
-    m->ctxA = cv.take<char>(R * h.ctx_len * h.ctx_dim, m->es);
-    m->kx = cv.take<char>(R * h.ctx_len * D, m->es);
-    m->vTx = cv.take<char>(R * D * m->ldvx, m->es);
+    const size_t NE = m->n_entries, per_row = (size_t)h.ctx_len * h.ctx_dim;
+    m->ctxA = cv.take<char>(NE * per_row, m->es);
+    m->ctx_keep = cv.take<float>(NE * per_row);
+    m->kx = cv.take<char>(NE * h.L * h.ctx_len * D, m->es);
+    m->vTx = cv.take<char>(NE * h.L * D * m->ldvx, m->es);
+    m->ctx_st = cv.take<sf::CtxState>(1);
   }
 }
 
@@ -421,14 +443,30 @@ int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows
     sf::EmbedArgs e{x, n_lat, m->W_pe, m->b_pe, m->pos, m->h, rows, (int)h.C, (int)h.H, (int)h.W, (int)h.p, D, N};
     return sf::launch_embed(e, s);
   }));
-  if (h.has_cross) {
-    const float* nctx = cond->null_ctx ? cond->null_ctx : cond->ctx;
-    SF_TRY(timed(m, SF_KC_CROSS, s, [&]() {
-      return sf::launch_ctx_assemble(m->bf16, cond->ctx, nctx, n_lat, rows, h.ctx_len, h.ctx_dim, m->ctxA, s);
-    }));
-  }
   const sf::FastDiv div_n = sf::make_fastdiv(N), div_d = sf::make_fastdiv(D), div_dh = sf::make_fastdiv(m->dh);
   const sf::FastDiv div_ctx = sf::make_fastdiv(h.has_cross ? h.ctx_len : 1);
+  const int* kv_map = nullptr;
+  if (h.has_cross) {
+    // the context entries of this call (reused or assembled), then the keys and values
+    // of every block for them in one GEMM; entries that are reused skip their tiles
+    const bool guided = rows > n_lat;
+    const sf::CtxArgs c{cond->ctx, guided ? cond->null_ctx : nullptr, n_lat, guided ? 1 : 0,
+                        (int)(h.ctx_len * h.ctx_dim), m->n_entries, m->ctx_keep, m->ctxA, m->ctx_st};
+    const char* st = (const char*)m->ctx_st;
+    kv_map = (const int*)(st + offsetof(sf::CtxState, kv_map));
+    SF_TRY(timed(m, SF_KC_CROSS, s, [&]() -> hipError_t {
+      const hipError_t e = m->ctx_cache_on ? sf::launch_ctx_lookup(m->bf16, c, s) : sf::launch_ctx_prepare(m->bf16, c, s);
+      if (e != hipSuccess) return e;
+      const int entries = m->ctx_cache_on ? m->n_entries : n_lat + (guided ? 1 : 0);
+      sf::GemmArgs g = gemm_base(m->ctxA, h.ctx_dim, m->W_kvx, h.ctx_dim, entries * h.ctx_len, 2 * D * h.L, h.ctx_dim,
+                                 m->b_kvx);
+      g.k = m->kx; g.vT = m->vTx; g.heads = h.heads; g.dh = m->dh; g.D = D; g.ntok = h.ctx_len;
+      g.ldv = m->ldvx; g.which_base = 1; g.vperm = m->vperm; g.kv_blocks = h.L;
+      g.div_ntok = div_ctx; g.div_D = div_d; g.div_dh = div_dh;
+      g.row_live = m->ctx_cache_on ? (const int*)(st + offsetof(sf::CtxState, live)) : nullptr;
+      return sf::launch_gemm(m->bf16, sf::EPI_KVX, g, s);
+    }));
+  }
   auto ln = [&](int shift_off, int scale_off, bool modulate) {
     sf::LnArgs a{m->h, m->act, M, D, modulate ? m->table : nullptr, m->modw, shift_off, scale_off, div_n, n_lat};
     return sf::launch_ln(m->bf16, a, s);
@@ -463,13 +501,14 @@ int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows
         gq.q = m->q; gq.heads = h.heads; gq.dh = m->dh; gq.D = D; gq.ntok = N; gq.which_base = 0; gq.vperm = m->vperm;
         gq.div_ntok = div_n; gq.div_D = div_d; gq.div_dh = div_dh;
         if ((e = sf::launch_gemm(m->bf16, sf::EPI_QKV, gq, s)) != hipSuccess) return e;
-        sf::GemmArgs gk = gemm_base(m->ctxA, h.ctx_dim, b.W_kvx, h.ctx_dim, rows * h.ctx_len, 2 * D, h.ctx_dim, b.b_kvx);
-        gk.k = m->kx; gk.vT = m->vTx; gk.heads = h.heads; gk.dh = m->dh; gk.D = D; gk.ntok = h.ctx_len;
-        gk.ldv = m->ldvx; gk.which_base = 1; gk.vperm = m->vperm;
-        gk.div_ntok = div_ctx; gk.div_D = div_d; gk.div_dh = div_dh;
-        if ((e = sf::launch_gemm(m->bf16, sf::EPI_QKV, gk, s)) != hipSuccess) return e;
-        sf::AttnArgs a{m->q, m->kx, m->vTx, m->o, rows, (int)h.heads, N, (int)h.ctx_len, m->dh, m->ldvx, D,
+        // row r reads entry kv_map[r], block l of it
+        const size_t kblk = (size_t)h.heads * h.ctx_len * m->dh, vblk = (size_t)h.heads * m->dh * m->ldvx;
+        sf::AttnArgs a{m->q, (const char*)m->kx + l * kblk * m->es, (const char*)m->vTx + l * vblk * m->es, m->o,
+                       rows, (int)h.heads, N, (int)h.ctx_len, m->dh, m->ldvx, D,
                        (float)(1.0 / std::sqrt((double)m->dh)), m->vperm};
+        a.kv_map = kv_map;
+        a.k_rs = h.L * kblk;
+        a.v_rs = h.L * vblk;
         if ((e = sf::launch_attention(m->bf16, a, s)) != hipSuccess) return e;
         sf::GemmArgs go = gemm_base(m->o, D, b.W_ox, D, M, D, D, b.b_ox);
         go.h = m->h; go.ldh = D;
@@ -544,6 +583,8 @@ bool modulation_cached(const sf_model* m, const float* t, int n, hipStream_t s) 
 // Records what a network call left in the table: the rows of t[0..n) if it computed them
 // (or reused them) and succeeded; nothing valid otherwise.
 int note_modulation(sf_model* m, const float* t, int n, hipStream_t s, int rc) {
+  // a failed call may have left the context entries half updated: forget them
+  if (rc != SF_OK && m->ctx_cache_on && m->ctx_st) (void)sf::launch_ctx_reset(m->ctx_st, s);
   m->mod_valid = rc == SF_OK;
   if (m->mod_valid) {
     m->mod_n = n;
@@ -562,7 +603,7 @@ void key_put(std::vector<char>& k, const T& v) {
   k.insert(k.end(), p, p + sizeof(T));
 }
 
-std::vector<char> call_key(int kind, const void* a, const void* b, const void* c, const void* d, int B,
+std::vector<char> call_key(const sf_model* m, int kind, const void* a, const void* b, const void* c, const void* d, int B,
                            const float* t, const float* dt, const sf_cond* cond, hipStream_t s,
                            bool table_ready) {
   std::vector<char> k;
@@ -579,6 +620,7 @@ std::vector<char> call_key(int kind, const void* a, const void* b, const void* c
     for (int i = 0; i < B; ++i) key_put(k, dt[i]);
   const bool has = cond != nullptr;
   key_put(k, has);
+  key_put(k, m->ctx_cache_on);
   if (has) {
     key_put(k, (const void*)cond->ctx);
     key_put(k, (const void*)cond->null_ctx);
@@ -686,6 +728,9 @@ int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows
   // workspace clear
   m->ldv = (m->N + 63) / 64 * 64;
   m->ldvx = h.has_cross ? (int)((h.ctx_len + 63) / 64 * 64) : 0;
+  // one entry per conditional row plus the null context (a call has at most max_rows
+  // context rows and one null row)
+  m->n_entries = h.has_cross ? max_rows + 1 : 0;
   m->vperm = m->bf16 ? 1 : 0;
 
   Carver cw;
@@ -777,7 +822,7 @@ int sf_velocity(sf_model* m, const float* x, const float* t, int B, const sf_con
   hipStream_t s = (hipStream_t)stream;
   const bool ready = modulation_cached(m, t, B, s);
   if (ready) ++m->mod_skips;
-  const int rc = run_graphed(m, call_key(0, x, v, nullptr, nullptr, B, t, nullptr, cond, s, ready), s, [&]() -> int {
+  const int rc = run_graphed(m, call_key(m, 0, x, v, nullptr, nullptr, B, t, nullptr, cond, s, ready), s, [&]() -> int {
     SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, guided ? m->vrows : v, s, ready));
     if (guided) return timed(m, SF_KC_EULER, s, [&]() { return sf::launch_cfg_combine(m->vrows, B, m->E, w, v, s); });
     return SF_OK;
@@ -797,7 +842,7 @@ int sf_stream_step(sf_model* m, float* x, const float* t, const float* dt, int B
   hipStream_t s = (hipStream_t)stream;
   const bool ready = modulation_cached(m, t, B, s);
   if (ready) ++m->mod_skips;
-  const int rc = run_graphed(m, call_key(1, x, z_new, x_done, nullptr, B, t, dt, cond, s, ready), s, [&]() -> int {
+  const int rc = run_graphed(m, call_key(m, 1, x, z_new, x_done, nullptr, B, t, dt, cond, s, ready), s, [&]() -> int {
     SF_TRY(run_network(m, x, t, B, rows, cond, m->hd.L, m->vrows, s, ready));
     return timed(m, SF_KC_EULER, s, [&]() {
       sf::EulerArgs a{};
@@ -930,6 +975,31 @@ int sf_modulation_cache(sf_model* m, int enable) {
   if (!m) return SF_E_NOTLOADED;
   m->mod_cache_on = enable != 0;
   m->mod_valid = false;
+  return SF_OK;
+}
+
+int sf_context_cache(sf_model* m, int enable) {
+  if (!m) return SF_E_NOTLOADED;
+  if (m->ctx_st) {
+    if (hipDeviceSynchronize() != hipSuccess || sf::launch_ctx_reset(m->ctx_st, nullptr) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess)
+      return SF_E_HIP;
+  }
+  m->ctx_cache_on = enable != 0;
+  return SF_OK;
+}
+
+int sf_context_cache_stats(const sf_model* m, long* calls, long* computed) {
+  if (!m) return SF_E_NOTLOADED;
+  if (!calls || !computed) return SF_E_INVAL;
+  *calls = 0;
+  *computed = 0;
+  if (!m->ctx_st) return SF_OK;
+  sf::CtxState st;
+  if (hipDeviceSynchronize() != hipSuccess || hipMemcpy(&st, m->ctx_st, sizeof(st), hipMemcpyDeviceToHost) != hipSuccess)
+    return SF_E_HIP;
+  *calls = (long)st.calls;
+  *computed = (long)st.computed;
   return SF_OK;
 }
 

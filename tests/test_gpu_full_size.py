@@ -99,6 +99,35 @@ def test_s512_cfg_guided_stream_step_parity():
     _step_and_check("s512_cfg", "bf16", cond)
 
 
+def test_s512_cfg_stream_step_with_context_reuse():
+    """The guided 512² step with the context entries kept across calls: the first call
+    projects the 8 contexts and the null one, the second reuses all of them; both
+    against the oracle, and bit-identical to the step without reuse."""
+    from paper_2511_22009_amd import Cond
+    cfg, x, t, dt = _inputs("s512_cfg")
+    cond = Cond(dev(W.context(cfg, cfg.K)), dev(W.null_context(cfg)), cfg.guidance)
+    m = model("s512_cfg", "bf16", max_rows=cfg.rows)
+    z = dev(W.z_new_for_image(cfg, 11))
+
+    def step():
+        xd = dev(x)
+        done = torch.empty(cfg.latent_shape, device="cuda")
+        m.stream_step(xd, t, dt, cfg.K, z, done, cond)
+        return host(xd), host(done)
+
+    plain = step()
+    m.context_cache(True)
+    try:
+        for _ in range(2):
+            got = step()
+            np.testing.assert_array_equal(got[0], plain[0])
+            np.testing.assert_array_equal(got[1], plain[1])
+        assert m.context_cache_stats() == (2, cfg.K + 1)
+    finally:
+        m.context_cache(False)
+    _step_and_check("s512_cfg", "bf16", cond)
+
+
 @pytest.mark.parametrize("blocks", [0, 1])
 def test_s1024_residual_stream_parity(blocks):
     cfg, x, t, _ = _inputs("s1024")
