@@ -71,7 +71,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const size_t bh = (size_t)r * a.heads + head;
   const size_t kr = a.kv_map ? (size_t)a.kv_map[r] : (size_t)r;  // the row whose keys and values r reads
   const bf16* Q = (const bf16*)a.q + bh * a.Nq * dh;
-  const bf16* Kg = (const bf16*)a.k + kr * a.k_rs + (size_t)head * a.Nk * dh;
+  const bf16* Kg = (const bf16*)a.k + kr * a.k_rs + (size_t)head * a.k_ld * dh;
   const bf16* Vt = (const bf16*)a.vT + kr * a.v_rs + (size_t)head * dh * a.ldv;
   const int qi = qblk * kQB + qg * 32 + l32;
 
@@ -304,7 +304,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   const size_t bh = (size_t)r * a.heads + head;
   const size_t kr = a.kv_map ? (size_t)a.kv_map[r] : (size_t)r;  // the row whose keys and values r reads
   const bf16* Q = (const bf16*)a.q + bh * a.Nq * DH;
-  const bf16* Kg = (const bf16*)a.k + kr * a.k_rs + (size_t)head * a.Nk * DH;
+  const bf16* Kg = (const bf16*)a.k + kr * a.k_rs + (size_t)head * a.k_ld * DH;
   const bf16* Vt = (const bf16*)a.vT + kr * a.v_rs + (size_t)head * DH * a.ldv;
   const int qi = qblk * kQB + qg * 32 + l32;
 
@@ -480,7 +480,7 @@ __global__ __launch_bounds__(128) void attn_f32_kernel(AttnArgs a) {
   const size_t bh = (size_t)r * a.heads + head;
   const size_t kr = a.kv_map ? (size_t)a.kv_map[r] : (size_t)r;  // the row whose keys and values r reads
   const float* Q = (const float*)a.q + bh * a.Nq * dh;
-  const float* Kg = (const float*)a.k + kr * a.k_rs + (size_t)head * a.Nk * dh;
+  const float* Kg = (const float*)a.k + kr * a.k_rs + (size_t)head * a.k_ld * dh;
   const float* Vt = (const float*)a.vT + kr * a.v_rs + (size_t)head * dh * a.ldv;
   const int qi = blockIdx.x * blockDim.x + threadIdx.x;
   float q[DHMAX], o[DHMAX];
@@ -536,7 +536,8 @@ static void launch_bf16_inst(const AttnArgs& a, hipStream_t s) {
 
 hipError_t launch_attention(bool use_bf16, const AttnArgs& args, hipStream_t s) {
   AttnArgs a = args;
-  if (!a.k_rs) a.k_rs = (size_t)a.heads * a.Nk * a.dh;
+  if (!a.k_ld) a.k_ld = a.Nk;
+  if (!a.k_rs) a.k_rs = (size_t)a.heads * a.k_ld * a.dh;
   if (!a.v_rs) a.v_rs = (size_t)a.heads * a.dh * a.ldv;
   if (!attention_supports(a.dh)) return hipErrorInvalidValue;
   // the bf16 kernels read transposed v in the permuted key layout only, with rows of

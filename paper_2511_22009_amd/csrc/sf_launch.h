@@ -101,7 +101,8 @@ struct CtxArgs {
   int per_row;            // ctx_len * ctx_dim
   int n_entries;          // entries held (max_rows + 1)
   float* keep;            // [n_entries][per_row]: the context each entry was computed from
-  void* ctxA;             // [n_entries][per_row]: the same in the compute type (GEMM operand)
+  void* ctxA;             // [n_entries][pitch]: the same in the compute type (GEMM operand);
+  int pitch;              // pitch = ctx_len rounded up to 16 tokens, x ctx_dim (zero rows)
   CtxState* st;
 };
 // Without reuse: entries 0..B-1 take the conditional contexts, entry B the null
@@ -203,10 +204,12 @@ struct AttnArgs {
   float scale;          // 1 / sqrt(dh)
   int vperm;
   // optional: row r reads the keys and values of row kv_map[r] (nullptr: row r), whose
-  // k starts k_rs elements after the previous row's and vT v_rs after (0: heads*Nk*dh
-  // and heads*dh*ldv, the packed layout)
+  // k starts k_rs elements after the previous row's and vT v_rs after (0: heads*k_ld*dh
+  // and heads*dh*ldv, the packed layout); k holds k_ld >= Nk key rows per head (0: Nk),
+  // the rows past Nk unread
   const int* kv_map;
   size_t k_rs, v_rs;
+  int k_ld;
 };
 hipError_t launch_attention(bool use_bf16, const AttnArgs& a, hipStream_t s);
 bool attention_supports(int dh);

@@ -111,6 +111,7 @@ struct sf_model {
   float* ctx_keep = nullptr;
   sf::CtxState* ctx_st = nullptr;
   int n_entries = 0;
+  int ctx_lp = 0;  // context tokens per entry in ctxA and kx: ctx_len rounded up to 16 (zero rows)
   bool ctx_cache_on = false;
   // every block's context K/V projection, contiguous: [L][2D][ctx_dim] and [L][2D]
   void* W_kvx = nullptr;
@@ -192,7 +193,8 @@ int check_capacity(const Header& h, int max_rows, size_t es) {
   if (R * N * widest * unit >= limit) return SF_E_UNSUPPORTED;
   // cross-attention: the context entries (max_rows + 1) and every block's K/V weights,
   // the operands of one GEMM
-  if (h.has_cross && ((R + 1) * h.ctx_len * (uint64_t)(h.ctx_dim > h.D ? h.ctx_dim : h.D) * unit >= limit ||
+  const uint64_t ctx_lp = ((uint64_t)h.ctx_len + 15) / 16 * 16;
+  if (h.has_cross && ((R + 1) * ctx_lp * (uint64_t)(h.ctx_dim > h.D ? h.ctx_dim : h.D) * unit >= limit ||
                       (uint64_t)h.L * 2 * h.D * h.ctx_dim * unit >= limit))
     return SF_E_UNSUPPORTED;
   return SF_OK;
@@ -266,9 +268,9 @@ void carve_workspace(sf_model* m, Carver& cv) {
   m->f = cv.take<char>(M * h.mlp, m->es);
   if (h.has_cross) {
     const size_t NE = m->n_entries, per_row = (size_t)h.ctx_len * h.ctx_dim;
-    m->ctxA = cv.take<char>(NE * per_row, m->es);
+    m->ctxA = cv.take<char>(NE * m->ctx_lp * h.ctx_dim, m->es);
     m->ctx_keep = cv.take<float>(NE * per_row);
-    m->kx = cv.take<char>(NE * h.L * h.ctx_len * D, m->es);
+    m->kx = cv.take<char>(NE * h.L * m->ctx_lp * D, m->es);
     m->vTx = cv.take<char>(NE * h.L * D * m->ldvx, m->es);
     m->ctx_st = cv.take<sf::CtxState>(1);
   }
@@ -444,23 +446,24 @@ int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows
     return sf::launch_embed(e, s);
   }));
   const sf::FastDiv div_n = sf::make_fastdiv(N), div_d = sf::make_fastdiv(D), div_dh = sf::make_fastdiv(m->dh);
-  const sf::FastDiv div_ctx = sf::make_fastdiv(h.has_cross ? h.ctx_len : 1);
+  const sf::FastDiv div_ctx = sf::make_fastdiv(h.has_cross ? m->ctx_lp : 1);
   const int* kv_map = nullptr;
   if (h.has_cross) {
     // the context entries of this call (reused or assembled), then the keys and values
     // of every block for them in one GEMM; entries that are reused skip their tiles
     const bool guided = rows > n_lat;
     const sf::CtxArgs c{cond->ctx, guided ? cond->null_ctx : nullptr, n_lat, guided ? 1 : 0,
-                        (int)(h.ctx_len * h.ctx_dim), m->n_entries, m->ctx_keep, m->ctxA, m->ctx_st};
+                        (int)(h.ctx_len * h.ctx_dim), m->n_entries, m->ctx_keep, m->ctxA,
+                        (int)(m->ctx_lp * h.ctx_dim), m->ctx_st};
     const char* st = (const char*)m->ctx_st;
     kv_map = (const int*)(st + offsetof(sf::CtxState, kv_map));
     SF_TRY(timed(m, SF_KC_CROSS, s, [&]() -> hipError_t {
       const hipError_t e = m->ctx_cache_on ? sf::launch_ctx_lookup(m->bf16, c, s) : sf::launch_ctx_prepare(m->bf16, c, s);
       if (e != hipSuccess) return e;
       const int entries = m->ctx_cache_on ? m->n_entries : n_lat + (guided ? 1 : 0);
-      sf::GemmArgs g = gemm_base(m->ctxA, h.ctx_dim, m->W_kvx, h.ctx_dim, entries * h.ctx_len, 2 * D * h.L, h.ctx_dim,
+      sf::GemmArgs g = gemm_base(m->ctxA, h.ctx_dim, m->W_kvx, h.ctx_dim, entries * m->ctx_lp, 2 * D * h.L, h.ctx_dim,
                                  m->b_kvx);
-      g.k = m->kx; g.vT = m->vTx; g.heads = h.heads; g.dh = m->dh; g.D = D; g.ntok = h.ctx_len;
+      g.k = m->kx; g.vT = m->vTx; g.heads = h.heads; g.dh = m->dh; g.D = D; g.ntok = m->ctx_lp;
       g.ldv = m->ldvx; g.which_base = 1; g.vperm = m->vperm; g.kv_blocks = h.L;
       g.div_ntok = div_ctx; g.div_D = div_d; g.div_dh = div_dh;
       g.row_live = m->ctx_cache_on ? (const int*)(st + offsetof(sf::CtxState, live)) : nullptr;
@@ -501,12 +504,13 @@ int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows
         gq.q = m->q; gq.heads = h.heads; gq.dh = m->dh; gq.D = D; gq.ntok = N; gq.which_base = 0; gq.vperm = m->vperm;
         gq.div_ntok = div_n; gq.div_D = div_d; gq.div_dh = div_dh;
         if ((e = sf::launch_gemm(m->bf16, sf::EPI_QKV, gq, s)) != hipSuccess) return e;
-        // row r reads entry kv_map[r], block l of it
-        const size_t kblk = (size_t)h.heads * h.ctx_len * m->dh, vblk = (size_t)h.heads * m->dh * m->ldvx;
+        // row r reads entry kv_map[r], block l of it (ctx_len keys of ctx_lp rows per head)
+        const size_t kblk = (size_t)h.heads * m->ctx_lp * m->dh, vblk = (size_t)h.heads * m->dh * m->ldvx;
         sf::AttnArgs a{m->q, (const char*)m->kx + l * kblk * m->es, (const char*)m->vTx + l * vblk * m->es, m->o,
                        rows, (int)h.heads, N, (int)h.ctx_len, m->dh, m->ldvx, D,
                        (float)(1.0 / std::sqrt((double)m->dh)), m->vperm};
         a.kv_map = kv_map;
+        a.k_ld = m->ctx_lp;
         a.k_rs = h.L * kblk;
         a.v_rs = h.L * vblk;
         if ((e = sf::launch_attention(m->bf16, a, s)) != hipSuccess) return e;
@@ -731,6 +735,9 @@ int sf_load_weights(const void* blob, size_t nbytes, int precision, int max_rows
   // one entry per conditional row plus the null context (a call has at most max_rows
   // context rows and one null row)
   m->n_entries = h.has_cross ? max_rows + 1 : 0;
+  // a context entry spans whole 16-token groups, so the transposed values of every
+  // 16 tokens leave the projection's epilogue as vector stores
+  m->ctx_lp = h.has_cross ? (int)((h.ctx_len + 15) / 16 * 16) : 0;
   m->vperm = m->bf16 ? 1 : 0;
 
   Carver cw;
