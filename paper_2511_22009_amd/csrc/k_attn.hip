@@ -34,7 +34,7 @@ constexpr float kLazy = 8.0f;  // max drift (exp2 units) tolerated before a resc
 // multiple of 32, so the last dh block has zero rows): row DB*32 - 8 of every V^T tile
 // is all ones, and the P.V MFMAs then also produce each query's probability sum in that
 // output row, which replaces the per-score additions of the row sum.
-template <int DHC, int DB, bool SUMROW>
+template <int DHC, int DB, bool SUMROW, int QB>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   constexpr int KLD = DHC * 16 + 8;     // K tile row pitch (bf16)
   constexpr int VLD = kKH + 8;          // V^T tile row pitch (bf16)
@@ -46,7 +46,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   constexpr int KCH = (KCHMAX + 255) / 256;
   constexpr int VCH = (VCHMAX + 255) / 256;
   constexpr int TILE_BYTES = 2 * 2 * (KT + VT) * 2;             // [buf][half] K and V^T
-  constexpr int MERGE_BYTES = 2 * 64 * (DB * 16 + 2) * 4;       // per query group: o, m, l
+  constexpr int MERGE_BYTES = 2 * 64 * (DB * 16 + 2) * 4;       // per query group: o, m, l (one block)
   constexpr int SMEM = (TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) + 16;  // + spare slot
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   bf16* const Ks = (bf16*)smem;                  // [buf][half][kKH][KLD]
@@ -59,7 +59,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   // Workgroup b runs on XCD b % 8. Give each XCD a contiguous range of (row, head,
   // query block) triples, query blocks fastest, so the query blocks that stream the same
   // K and V share one L2.
-  const int nqb = (a.Nq + kQB - 1) / kQB;
+  constexpr int QPW = QB * 64;  // queries per workgroup
+  const int nqb = (a.Nq + QPW - 1) / QPW;
   const int T = nqb * a.heads * a.rows;
   const int xcd = blockIdx.x % 8, local = blockIdx.x / 8;
   const int base = T / 8, rem = T % 8;
@@ -73,20 +74,24 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const bf16* Q = (const bf16*)a.q + bh * a.Nq * dh;
   const bf16* Kg = (const bf16*)a.k + kr * a.k_rs + (size_t)head * a.k_ld * dh;
   const bf16* Vt = (const bf16*)a.vT + kr * a.v_rs + (size_t)head * dh * a.ldv;
-  const int qi = qblk * kQB + qg * 32 + l32;
+  int qi[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) qi[qb] = qblk * QPW + qg * 32 * QB + qb * 32 + l32;
 
   // zero the tile buffers once: padding columns (dh..KLD) and rows (dh..VROWS) are
   // never written by the staging
   for (int i = tid; i < TILE_BYTES / 16; i += 256) ((u32x4*)smem)[i] = u32x4{0u, 0u, 0u, 0u};
 
-  bf16x8 qf[DHC];
+  bf16x8 qf[QB][DHC];
   const __amdgpu_buffer_rsrc_t q_src = buffer_rsrc(Q, (uint32_t)a.Nq * dh * 2);
 #pragma unroll
-  for (int kk = 0; kk < DHC; ++kk) {
-    const int d0 = kk * 16 + g * 8;
-    const u32x4 w = buffer_load16(q_src, (qi < a.Nq && d0 < dh) ? (qi * dh + d0) * 2 : kOffOOB);
-    qf[kk] = __builtin_bit_cast(bf16x8, w);
-  }
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int kk = 0; kk < DHC; ++kk) {
+      const int d0 = kk * 16 + g * 8;
+      const u32x4 w = buffer_load16(q_src, (qi[qb] < a.Nq && d0 < dh) ? (qi[qb] * dh + d0) * 2 : kOffOOB);
+      qf[qb][kk] = __builtin_bit_cast(bf16x8, w);
+    }
 
   // staging map, fixed per thread: K chunk c = (key 0..63, 16-byte column); V^T chunk
   // c = (dh row, 8-key column group 0..7). Chunks past the real count read zeros and
@@ -131,12 +136,19 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     for (int i = 0; i < VCH; ++i) *(u32x4*)&Vs[v_lds[i] >= 0 ? buf * 2 * VT + v_lds[i] : SPARE - 4 * KT] = rv[i];
   };
 
-  f32x16 o[DB];
+  f32x16 o[QB][DB];
 #pragma unroll
-  for (int b = 0; b < DB; ++b)
+  for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) o[b][e] = 0.0f;
-  float m2 = -INFINITY, lsum = 0.0f;               // running max in exp2 units, partial sum
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[qb][b][e] = 0.0f;
+  float m2[QB], lsum[QB];                          // running max in exp2 units, partial sum
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    m2[qb] = -INFINITY;
+    lsum[qb] = 0.0f;
+  }
   const float sl2 = a.scale * 1.4426950408889634f;  // scores -> exp2 units
 
   const int nsteps = (a.Nk + 2 * kKH - 1) / (2 * kKH);
@@ -163,43 +175,52 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     // tail of the last step) contributes nothing: its scores would all be -inf, and a
     // wavefront that has seen no key yet would take exp2(-inf + inf)
     if (kv0 < a.Nk) {
-      f32x16 s;
+      // every K and V^T fragment feeds the MFMAs of all QB query blocks
+      f32x16 s[QB];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) s[e] = 0.0f;
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s[qb][e] = 0.0f;
 #pragma unroll
       for (int kk = 0; kk < DHC; ++kk) {
         const bf16x8 kf = *(const bf16x8*)&Kb[l32 * KLD + kk * 16 + g * 8];
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][kk], s[qb], 0, 0, 0);
       }
-      // s[e]: query l32, key kv0 + (e/4)*8 + g*4 + e%4, raw (unscaled). Only the last,
-      // ragged step needs the key mask.
+      // s[qb][e]: query l32 of block qb, key kv0 + (e/4)*8 + g*4 + e%4, raw (unscaled).
+      // Only the last, ragged step needs the key mask.
       if (kv0 + kKH > a.Nk) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e)
-          if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) s[e] = -INFINITY;
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) s[qb][e] = -INFINITY;
       }
-      float tmax = s[0];
+      bf16x8 pf[QB][2];
 #pragma unroll
-      for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, s[e]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
-      if (__any(tmax > m2 + kLazy)) {
-        const float mnew = fmaxf(m2, tmax);
-        const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
-        lsum *= alpha;
+      for (int qb = 0; qb < QB; ++qb) {
+        float tmax = s[qb][0];
 #pragma unroll
-        for (int b = 0; b < DB; ++b)
+        for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, s[qb][e]);
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+        if (__any(tmax > m2[qb] + kLazy)) {
+          const float mnew = fmaxf(m2[qb], tmax);
+          const float alpha = __builtin_amdgcn_exp2f(m2[qb] - mnew);
+          lsum[qb] *= alpha;
 #pragma unroll
-          for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
-        m2 = mnew;
-      }
-      bf16x8 pf[2];
+          for (int b = 0; b < DB; ++b)
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+            for (int e = 0; e < 16; ++e) o[qb][b][e] *= alpha;
+          m2[qb] = mnew;
+        }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[ks * 8 + j], sl2, -m2));
-          if constexpr (!SUMROW) lsum += p;
-          pf[ks][j] = (bf16)p;
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float p = __builtin_amdgcn_exp2f(fmaf(s[qb][ks * 8 + j], sl2, -m2[qb]));
+            if constexpr (!SUMROW) lsum[qb] += p;
+            pf[qb][ks][j] = (bf16)p;
+          }
         }
       }
       // V^T fragment of k-slots 8g..8g+7 (keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
@@ -209,7 +230,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           const bf16x8 vf = *(const bf16x8*)&Vb[(b * 32 + l32) * VLD + ks * 16 + g * 8];
-          o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            o[qb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb][ks], o[qb][b], 0, 0, 0);
         }
       }
     }
@@ -219,44 +242,52 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 
   // the ones row's output (row kSumRow of the last block: register 12 of lane half 0;
   // lane half 1 holds row kSumRow + 4, a zero row) is this wavefront's probability sum
-  if constexpr (SUMROW) lsum = o[DB - 1][12];
-  // merge the key halves: half 1 hands (o, max, partial sum) to half 0 through LDS
-  float* mg = (float*)smem + qg * 64 * (DB * 16 + 2);
-  if (kh == 1) {
+  if constexpr (SUMROW) {
 #pragma unroll
-    for (int b = 0; b < DB; ++b)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mg[(b * 16 + e) * 64 + lane] = o[b][e];
-    mg[DB * 16 * 64 + lane] = m2;
-    mg[(DB * 16 + 1) * 64 + lane] = lsum;
+    for (int qb = 0; qb < QB; ++qb) lsum[qb] = o[qb][DB - 1][12];
   }
-  __syncthreads();
-  if (kh == 1) return;
-  const float m2b = mg[DB * 16 * 64 + lane];
-  const float mnew = fmaxf(m2, m2b);
-  const float a0 = m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2 - mnew);
-  const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
-  // a half that saw no key (max still -inf) holds zeros and is left out by selects,
-  // not multiplied by a zero weight
-  const bool own = m2 != -INFINITY, other = m2b != -INFINITY;
-  lsum = (own ? lsum * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
-  lsum += __shfl_xor(lsum, 32);
-  const float inv = 1.0f / lsum;
-  if (qi < a.Nq) {
-    bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi) * a.D + (size_t)head * dh;
+  // merge the key halves one query block at a time: half 1 hands (o, max, partial sum)
+  // to half 0 through LDS
+  float* mg = (float*)smem + qg * 64 * (DB * 16 + 2);
 #pragma unroll
-    for (int b = 0; b < DB; ++b)
+  for (int qb = 0; qb < QB; ++qb) {
+    if (qb > 0) __syncthreads();  // the previous block's values were read
+    if (kh == 1) {
 #pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        const int d = b * 32 + e4 * 8 + g * 4;
-        float w[4];
+      for (int b = 0; b < DB; ++b)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int e = e4 * 4 + q;
-          w[q] = ((own ? o[b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
+        for (int e = 0; e < 16; ++e) mg[(b * 16 + e) * 64 + lane] = o[qb][b][e];
+      mg[DB * 16 * 64 + lane] = m2[qb];
+      mg[(DB * 16 + 1) * 64 + lane] = lsum[qb];
+    }
+    __syncthreads();
+    if (kh == 1) continue;
+    const float m2b = mg[DB * 16 * 64 + lane];
+    const float mnew = fmaxf(m2[qb], m2b);
+    const float a0 = m2[qb] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2[qb] - mnew);
+    const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
+    // a half that saw no key (max still -inf) holds zeros and is left out by selects,
+    // not multiplied by a zero weight
+    const bool own = m2[qb] != -INFINITY, other = m2b != -INFINITY;
+    float ls = (own ? lsum[qb] * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
+    ls += __shfl_xor(ls, 32);
+    const float inv = 1.0f / ls;
+    if (qi[qb] < a.Nq) {
+      bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi[qb]) * a.D + (size_t)head * dh;
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int d = b * 32 + e4 * 8 + g * 4;
+          float w[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int e = e4 * 4 + q;
+            w[q] = ((own ? o[qb][b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
+          }
+          if (d < dh) *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
         }
-        if (d < dh) *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
-      }
+    }
   }
 }
 
@@ -468,6 +499,221 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   }
 }
 
+// Head dim 64 with two 32-query blocks per wavefront: a workgroup owns 128 queries of
+// one (row, head) (two query groups of 64 times two key halves), and every K and V^T
+// fragment read from LDS feeds the MFMAs of both query blocks, half the LDS reads per
+// FLOP of attn_bf16_dma64_kernel, with two independent score / softmax chains per step
+// for the scheduler to interleave. Staging (three DMA stages of 64 keys) and each
+// query's arithmetic, in order, are those of attn_bf16_dma64_kernel.
+constexpr int kQB2 = 128;  // queries per workgroup
+
+__global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
+  constexpr int DH = 64, DHC = 4, DB = 2, CPR = 8, QB = 2;
+  constexpr int KCHUNKS = 2 * kKH * CPR;  // 512
+  constexpr int SB = (KCHUNKS + DH * CPR) * 16;
+  constexpr int LPT = SB / 16 / 256;  // loads per thread and step
+  constexpr int MERGE = 64 * (DB * 16 + 2) * 4;  // one query block of one query group
+  static_assert(MERGE <= SB && LPT == 4, "stage layout");
+  __shared__ __attribute__((aligned(16))) char st0[SB];
+  __shared__ __attribute__((aligned(16))) char st1[SB];
+  __shared__ __attribute__((aligned(16))) char st2[SB];
+  auto stage = [&](auto s) -> char* {
+    constexpr int S = decltype(s)::value % kAttnStages;
+    if constexpr (S == 0) return st0;
+    else if constexpr (S == 1) return st1;
+    else return st2;
+  };
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qg = wave & 1, kh = wave >> 1;
+  const int l32 = lane & 31, g = lane >> 5;
+  const int nqb = (a.Nq + kQB2 - 1) / kQB2;
+  const int T = nqb * a.heads * a.rows;
+  const int xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  const int base = T / 8, rem = T % 8;
+  const int logical = xcd * base + min(xcd, rem) + local;
+  const int qblk = logical % nqb;
+  const int rh = logical / nqb;
+  const int head = rh % a.heads, r = rh / a.heads;
+  const size_t bh = (size_t)r * a.heads + head;
+  const size_t kr = a.kv_map ? (size_t)a.kv_map[r] : (size_t)r;
+  const bf16* Q = (const bf16*)a.q + bh * a.Nq * DH;
+  const bf16* Kg = (const bf16*)a.k + kr * a.k_rs + (size_t)head * a.k_ld * DH;
+  const bf16* Vt = (const bf16*)a.vT + kr * a.v_rs + (size_t)head * DH * a.ldv;
+  int qi[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) qi[qb] = qblk * kQB2 + qg * 64 + qb * 32 + l32;
+
+  bf16x8 qf[QB][DHC];
+  const __amdgpu_buffer_rsrc_t q_src = buffer_rsrc(Q, (uint32_t)a.Nq * DH * 2);
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int kk = 0; kk < DHC; ++kk) {
+      const u32x4 w = buffer_load16(q_src, qi[qb] < a.Nq ? (qi[qb] * DH + kk * 16 + g * 8) * 2 : kOffOOB);
+      qf[qb][kk] = __builtin_bit_cast(bf16x8, w);
+    }
+
+  int goff[LPT];
+#pragma unroll
+  for (int i = 0; i < LPT; ++i) {
+    const int p = i * 256 + tid;
+    const int row = (p / CPR) % 64;
+    const int c = (p % CPR) ^ dma_swz<CPR>(row);
+    goff[i] = i < 2 ? (row * DH + c * 8) * 2 : (row * a.ldv + c * 8) * 2;
+  }
+  auto issue = [&](char* sb, int step) {
+    const int kv0 = step * 2 * kKH;
+    const __amdgpu_buffer_rsrc_t k_src =
+        buffer_rsrc(Kg + (size_t)kv0 * DH, (uint32_t)max(a.Nk - kv0, 0) * DH * 2);
+    const __amdgpu_buffer_rsrc_t v_src = buffer_rsrc(Vt + kv0, (uint32_t)max(DH * a.ldv - kv0, 0) * 2);
+#pragma unroll
+    for (int i = 0; i < LPT; ++i)
+      buffer_load16_lds(i < 2 ? k_src : v_src, sb + (i * 256 + wave * 64) * 16, goff[i]);
+  };
+
+  f32x16 o[QB][DB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[qb][b][e] = 0.0f;
+  float m2[QB], lsum[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    m2[qb] = -INFINITY;
+    lsum[qb] = 0.0f;
+  }
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const int sw = dma_swz<CPR>(l32);
+  const int krow = (kh * kKH + l32) * CPR;
+
+  constexpr int kWait = waitcnt_vm_lgkm0<(kAttnStages - 2) * LPT>();
+  auto step = [&](auto s, int it) {
+    constexpr int S = decltype(s)::value;
+    __builtin_amdgcn_s_waitcnt(kWait);
+    bare_barrier();
+    issue(stage(std::integral_constant<int, S + kAttnStages - 1>{}), it + kAttnStages - 1);
+    const char* cur = stage(std::integral_constant<int, S>{});
+    const int kv0 = it * 2 * kKH + kh * kKH;
+    if (kv0 >= a.Nk) return;
+    f32x16 sc[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[qb][e] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < DHC; ++kk) {
+      const bf16x8 kf = *(const bf16x8*)(cur + (krow + ((kk * 2 + g) ^ sw)) * 16);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][kk], sc[qb], 0, 0, 0);
+    }
+    if (kv0 + kKH > a.Nk) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) sc[qb][e] = -INFINITY;
+    }
+    bf16x8 pf[QB][2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float tmax = sc[qb][0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[qb][e]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+      if (__any(tmax > m2[qb] + kLazy)) {
+        const float mnew = fmaxf(m2[qb], tmax);
+        const float alpha = __builtin_amdgcn_exp2f(m2[qb] - mnew);
+        lsum[qb] *= alpha;
+#pragma unroll
+        for (int b = 0; b < DB; ++b)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[qb][b][e] *= alpha;
+        m2[qb] = mnew;
+      }
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(sc[qb][ks * 8 + j], sl2, -m2[qb]));
+          lsum[qb] += p;
+          pf[qb][ks][j] = (bf16)p;
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < DB; ++b) {
+      const char* vrow = cur + KCHUNKS * 16 + (b * 32 + l32) * CPR * 16;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x8 vf = *(const bf16x8*)(vrow + (((kh * 4 + 2 * ks + g) ^ sw) << 4));
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          o[qb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb][ks], o[qb][b], 0, 0, 0);
+      }
+    }
+  };
+
+  const int nsteps = (a.Nk + 2 * kKH - 1) / (2 * kKH);
+  issue(stage(std::integral_constant<int, 0>{}), 0);
+  issue(stage(std::integral_constant<int, 1>{}), 1);
+  int it = 0;
+  for (; it + kAttnStages <= nsteps; it += kAttnStages) {
+    step(std::integral_constant<int, 0>{}, it);
+    step(std::integral_constant<int, 1>{}, it + 1);
+    step(std::integral_constant<int, 2>{}, it + 2);
+  }
+  if (it < nsteps) step(std::integral_constant<int, 0>{}, it);
+  if (it + 1 < nsteps) step(std::integral_constant<int, 1>{}, it + 1);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  // merge the key halves one query block at a time: half 1 hands (o, max, partial sum)
+  // to half 0 through LDS (stage 0 for query group 0, stage 1 for query group 1)
+  float* mg = (float*)(qg == 0 ? st0 : st1);
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    if (qb > 0) __syncthreads();  // the previous block's values were read
+    if (kh == 1) {
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mg[(b * 16 + e) * 64 + lane] = o[qb][b][e];
+      mg[DB * 16 * 64 + lane] = m2[qb];
+      mg[(DB * 16 + 1) * 64 + lane] = lsum[qb];
+    }
+    __syncthreads();
+    if (kh == 0) {
+      const float m2b = mg[DB * 16 * 64 + lane];
+      const float mnew = fmaxf(m2[qb], m2b);
+      const float a0 = m2[qb] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2[qb] - mnew);
+      const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
+      const bool own = m2[qb] != -INFINITY, other = m2b != -INFINITY;
+      float ls = (own ? lsum[qb] * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
+      ls += __shfl_xor(ls, 32);
+      const float inv = 1.0f / ls;
+      if (qi[qb] < a.Nq) {
+        bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi[qb]) * a.D + (size_t)head * DH;
+#pragma unroll
+        for (int b = 0; b < DB; ++b)
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4) {
+            const int d = b * 32 + e4 * 8 + g * 4;
+            float w[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int e = e4 * 4 + q;
+              w[q] = ((own ? o[qb][b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
+            }
+            *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
+          }
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ fp32
 constexpr int kFKV = 32;
 
@@ -526,12 +772,20 @@ __global__ __launch_bounds__(128) void attn_f32_kernel(AttnArgs a) {
 bool attention_supports(int dh) { return dh >= 8 && dh <= 128 && dh % 8 == 0; }
 
 template <int DHC, int DB>
-static void launch_bf16_inst(const AttnArgs& a, hipStream_t s) {
+static void launch_bf16_inst(const AttnArgs& a, bool two_blocks, hipStream_t s) {
+  if (two_blocks) {
+    dim3 grid(((a.Nq + 2 * kQB - 1) / (2 * kQB)) * a.heads * a.rows);
+    if (a.dh % 32 != 0)
+      launch((attn_bf16_kernel<DHC, DB, true, 2>), grid, dim3(256), 0, s, a);
+    else
+      launch((attn_bf16_kernel<DHC, DB, false, 2>), grid, dim3(256), 0, s, a);
+    return;
+  }
   dim3 grid(((a.Nq + kQB - 1) / kQB) * a.heads * a.rows);
   if (a.dh % 32 != 0)
-    launch((attn_bf16_kernel<DHC, DB, true>), grid, dim3(256), 0, s, a);
+    launch((attn_bf16_kernel<DHC, DB, true, 1>), grid, dim3(256), 0, s, a);
   else
-    launch((attn_bf16_kernel<DHC, DB, false>), grid, dim3(256), 0, s, a);
+    launch((attn_bf16_kernel<DHC, DB, false, 1>), grid, dim3(256), 0, s, a);
 }
 
 hipError_t launch_attention(bool use_bf16, const AttnArgs& args, hipStream_t s) {
@@ -544,21 +798,28 @@ hipError_t launch_attention(bool use_bf16, const AttnArgs& args, hipStream_t s) 
   // whole 64-key steps; the fp32 kernel reads the plain layout
   if ((a.vperm != 0) != use_bf16 || (a.vperm && a.ldv % 64 != 0)) return hipErrorInvalidValue;
   if (use_bf16) {
+    // Two query blocks per wavefront (128 queries per workgroup) halve the LDS reads per
+    // FLOP but need two such workgroups per CU to fill the chip: taken when the layer
+    // has at least 512 of them. Both forms compute every query in the same order (the
+    // same bits), so the choice changes no result.
+    const bool two = (size_t)((a.Nq + 2 * kQB - 1) / (2 * kQB)) * a.heads * a.rows >= 512;
     const int dhc = (a.dh + 15) / 16;
     switch (dhc) {
-      case 1: launch_bf16_inst<1, 1>(a, s); break;
-      case 2: launch_bf16_inst<2, 1>(a, s); break;
-      case 3: launch_bf16_inst<3, 2>(a, s); break;
+      case 1: launch_bf16_inst<1, 1>(a, two, s); break;
+      case 2: launch_bf16_inst<2, 1>(a, two, s); break;
+      case 3: launch_bf16_inst<3, 2>(a, two, s); break;
       case 4:
-        if (a.dh == 64)
+        if (a.dh == 64 && two)
+          launch(attn_bf16_dma64x2_kernel, dim3(((a.Nq + kQB2 - 1) / kQB2) * a.heads * a.rows), dim3(256), 0, s, a);
+        else if (a.dh == 64)
           launch(attn_bf16_dma64_kernel, dim3(((a.Nq + kQB - 1) / kQB) * a.heads * a.rows), dim3(256), 0, s, a);
         else
-          launch_bf16_inst<4, 2>(a, s);
+          launch_bf16_inst<4, 2>(a, two, s);
         break;
-      case 5: launch_bf16_inst<5, 3>(a, s); break;
-      case 6: launch_bf16_inst<6, 3>(a, s); break;
-      case 7: launch_bf16_inst<7, 4>(a, s); break;
-      case 8: launch_bf16_inst<8, 4>(a, s); break;
+      case 5: launch_bf16_inst<5, 3>(a, two, s); break;
+      case 6: launch_bf16_inst<6, 3>(a, two, s); break;
+      case 7: launch_bf16_inst<7, 4>(a, two, s); break;
+      case 8: launch_bf16_inst<8, 4>(a, two, s); break;
       default: return hipErrorInvalidValue;
     }
   } else {
