@@ -84,6 +84,19 @@ def test_s512_heterogeneous_batch_equals_each_slot_alone():
         np.testing.assert_array_equal(full[k], host(m.velocity(dev(x[k:k + 1]), t[k:k + 1]))[0])
 
 
+def test_s512_eight_rows_equal_each_row_alone():
+    """Eight rows of the 512^2 network (768 attention workgroups of 128 queries: two
+    32-query blocks per wavefront, head dim 64) against each row alone (one block per
+    wavefront): the same bits."""
+    cfg = W.get_config("s512")
+    x = W.latents(cfg, 8, seed=77)
+    t = np.random.default_rng(78).uniform(0.0, 1.0, 8).astype(np.float32)
+    m = model("s512", "bf16", max_rows=8)
+    full = host(m.velocity(dev(x), t))
+    for k in range(8):
+        np.testing.assert_array_equal(full[k], host(m.velocity(dev(x[k:k + 1]), t[k:k + 1]))[0])
+
+
 def test_s512_large_velocity_parity():
     cfg, x, t, _ = _inputs("s512_large")
     got = host(model("s512_large", "bf16", max_rows=cfg.rows).velocity(dev(x), t))

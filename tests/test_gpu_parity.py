@@ -363,6 +363,20 @@ def test_max_rows_velocity_parity(name, prec):
     assert max(errs) <= TOL[prec], max(errs)
 
 
+def test_two_query_blocks_per_wavefront_equal_one():
+    """64 rows of the head-dim-48 network run attention with two 32-query blocks per
+    wavefront (512 workgroups of 128 queries); four rows at a time take one block per
+    wavefront. Every query is computed in the same order either way: same bits."""
+    cfg = W.get_config("ragged")
+    B = 64
+    x = W.latents(cfg, B, seed=75)
+    t = np.random.default_rng(76).uniform(0.0, 1.0, B).astype(np.float32)
+    m = model("ragged", "bf16", max_rows=B)
+    full = host(m.velocity(dev(x), t))
+    for k0 in range(0, B, 4):
+        np.testing.assert_array_equal(full[k0:k0 + 4], host(m.velocity(dev(x[k0:k0 + 4]), t[k0:k0 + 4])))
+
+
 @pytest.mark.parametrize("prec", PRECS)
 def test_max_rows_guided_velocity_parity(prec):
     """32 text-conditioned samples with guidance fill all 64 rows (cond and uncond)."""
