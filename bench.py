@@ -46,17 +46,17 @@ MI355X_HBM_GBS = 8000.0
 # only for the kernel sources it was measured on (hash below); otherwise traffic is null.
 KERNEL_SOURCES = ("k_gemm.hip", "k_attn.hip", "sf_device.h", "sf_launch.h")
 TRAFFIC = {
-    ("s512", "bf16", "FC2"): {"bytes": 94526502, "sources": "78b1dbc3f88e66e0",
+    ("s512", "bf16", "FC2"): {"bytes": 94522405, "sources": "e634ccf7e5fca853",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512", "bf16", "FC1"): {"bytes": 59973646, "sources": "78b1dbc3f88e66e0",
+    ("s512", "bf16", "FC1"): {"bytes": 59973659, "sources": "e634ccf7e5fca853",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512_large", "bf16", "FC2"): {"bytes": 185954085, "sources": "78b1dbc3f88e66e0",
+    ("s512_large", "bf16", "FC2"): {"bytes": 185915855, "sources": "e634ccf7e5fca853",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_large", "bf16", "FC1"): {"bytes": 132518135, "sources": "78b1dbc3f88e66e0",
+    ("s512_large", "bf16", "FC1"): {"bytes": 132230923, "sources": "e634ccf7e5fca853",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_cfg", "bf16", "FC2"): {"bytes": 389477503, "sources": "78b1dbc3f88e66e0",
+    ("s512_cfg", "bf16", "FC2"): {"bytes": 381436650, "sources": "e634ccf7e5fca853",
                                   "profile": "profiles/stream_step_s512_cfg_bf16.md"},
-    ("s1024", "bf16", "ATTN"): {"bytes": 166791190, "sources": "78b1dbc3f88e66e0",
+    ("s1024", "bf16", "ATTN"): {"bytes": 161664252, "sources": "e634ccf7e5fca853",
                                 "profile": "profiles/stream_step_s1024_bf16.md"},
 }
 
