@@ -268,18 +268,25 @@ def main():
             torch.cuda.synchronize()
             for i in range(pool.shape[0] + max(2, args.warmup)):
                 fn(i)
-            gmarks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+            # the timed steps carry no per-step events (an event between two graph
+            # launches adds a few microseconds to every step); the median step comes
+            # from a separate pass with an event before every step
             torch.cuda.synchronize()
             g0 = time.perf_counter()
             for i in range(args.steps):
-                gmarks[i].record(gs)
                 fn(i)
-            gmarks[-1].record(gs)
             torch.cuda.synchronize()
             gel = time.perf_counter() - g0
             if not bool(torch.isfinite(x).all()):
                 raise RuntimeError("non-finite latents after the graph-replay steps")
-            g_steps = sorted(gmarks[i].elapsed_time(gmarks[i + 1]) for i in range(args.steps))
+            n_med = min(args.steps, 20)
+            gmarks = [torch.cuda.Event(enable_timing=True) for _ in range(n_med + 1)]
+            for i in range(n_med):
+                gmarks[i].record(gs)
+                fn(i)
+            gmarks[-1].record(gs)
+            torch.cuda.synchronize()
+            g_steps = sorted(gmarks[i].elapsed_time(gmarks[i + 1]) for i in range(n_med))
             return {"ms_per_step": 1e3 * gel / args.steps, "latent_steps_per_s": K / (gel / args.steps),
                     "median_ms_per_step": g_steps[len(g_steps) // 2]}
 
