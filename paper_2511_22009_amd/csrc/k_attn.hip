@@ -714,6 +714,261 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
   }
 }
 
+// Head dim 72 with two 32-query blocks per wavefront, K and V^T moved by buffer_load ...
+// lds into a ring of three LDS stages two steps ahead, as attn_bf16_dma64_kernel does for
+// head dim 64. A stage holds the step's 64 keys:
+//  * K as 64 rows of 144 bytes (9 chunks). Consecutive rows then start 16 bytes apart
+//    modulo 128, so the fragment reads are conflict-free without a swizzle, and the
+//    stage is a byte copy of the step's contiguous K block.
+//  * V^T as 72 dh rows x 8 chunks (keys, permuted layout), swizzled with dma_swz.
+//  * 24 constant rows up to the 96 rows of the three dh blocks: zeros, and the ones row
+//    (row 88) whose P.V output is each query's probability sum. They are written once,
+//    before the first step; the loads never touch them.
+// The K fragment of dh 72..79 (the second half of the fifth 16-wide chunk) is a zero
+// register, like the zero padding of attn_bf16_kernel's K tile, and the queries' dh
+// 72..79 are zero too. Every query's arithmetic, in order, is that of
+// attn_bf16_kernel<5, 3, true, 2>, so both return the same bits.
+constexpr int kD72K = 64 * 9;                    // 16-byte K chunks per stage
+constexpr int kD72V = 72 * 8;                    // 16-byte V^T chunks per stage
+constexpr int kD72Stage = (kD72K + 96 * 8) * 16;  // + the constant rows: 21 KB
+__shared__ __attribute__((aligned(16))) char g_attn72_st0[kD72Stage];
+__shared__ __attribute__((aligned(16))) char g_attn72_st1[kD72Stage];
+__shared__ __attribute__((aligned(16))) char g_attn72_st2[kD72Stage];
+__shared__ __attribute__((aligned(16))) char g_attn72_spare[1024];
+
+__global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
+  constexpr int DH = 72, DHC = 5, DB = 3, QB = 2;
+  constexpr int NCH = kD72K + kD72V;         // 1152 chunks per step
+  constexpr int LPT = (NCH + 255) / 256;     // 5 loads per thread (128 of them spare)
+  constexpr int V_OFF = kD72K * 16;          // byte offset of V^T in a stage
+  constexpr int MERGE = 64 * (DB * 16 + 2) * 4;
+  static_assert(MERGE <= kD72Stage && NCH % 64 == 0, "stage layout");
+  constexpr int kSumRow = DB * 32 - 8;
+  char* const st0 = g_attn72_st0;
+  char* const st1 = g_attn72_st1;
+  char* const st2 = g_attn72_st2;
+  auto stage = [&](auto s) -> char* {
+    constexpr int S = decltype(s)::value % kAttnStages;
+    if constexpr (S == 0) return st0;
+    else if constexpr (S == 1) return st1;
+    else return st2;
+  };
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qg = wave & 1, kh = wave >> 1;
+  const int l32 = lane & 31, g = lane >> 5;
+  // each XCD (workgroup b runs on XCD b % 8) takes a contiguous range of (row, head,
+  // query block) triples, query blocks fastest, so the blocks of one (row, head) share
+  // an L2
+  const int nqb = (a.Nq + kQB2 - 1) / kQB2;
+  const int T = nqb * a.heads * a.rows;
+  const int xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  const int base = T / 8, rem = T % 8;
+  const int logical = xcd * base + min(xcd, rem) + local;
+  const int qblk = logical % nqb;
+  const int rh = logical / nqb;
+  const int head = rh % a.heads, r = rh / a.heads;
+  const size_t bh = (size_t)r * a.heads + head;
+  const size_t kr = a.kv_map ? (size_t)a.kv_map[r] : (size_t)r;
+  const bf16* Q = (const bf16*)a.q + bh * a.Nq * DH;
+  const bf16* Kg = (const bf16*)a.k + kr * a.k_rs + (size_t)head * a.k_ld * DH;
+  const bf16* Vt = (const bf16*)a.vT + kr * a.v_rs + (size_t)head * DH * a.ldv;
+  int qi[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) qi[qb] = qblk * kQB2 + qg * 64 + qb * 32 + l32;
+
+  // the constant rows 72..95 of every stage's V^T: zeros, ones in row kSumRow
+  for (int i = tid; i < kAttnStages * 24 * 8; i += 256) {
+    const int st = i / (24 * 8), c = i - st * (24 * 8), row = 72 + c / 8;
+    char* base = st == 0 ? st0 : st == 1 ? st1 : st2;
+    const uint32_t w = row == kSumRow ? 0x3F803F80u : 0u;
+    *(u32x4*)(base + V_OFF + (row * 8 + c % 8) * 16) = u32x4{w, w, w, w};
+  }
+
+  bf16x8 qf[QB][DHC];
+  const __amdgpu_buffer_rsrc_t q_src = buffer_rsrc(Q, (uint32_t)a.Nq * DH * 2);
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int kk = 0; kk < DHC; ++kk) {
+      const int d0 = kk * 16 + g * 8;
+      const u32x4 w = buffer_load16(q_src, (qi[qb] < a.Nq && d0 < DH) ? (qi[qb] * DH + d0) * 2 : kOffOOB);
+      qf[qb][kk] = __builtin_bit_cast(bf16x8, w);
+    }
+
+  // load i of a thread fills chunk position p = i * 256 + tid of a stage: K chunk p
+  // (bytes 16 p of the step's K block) for p < 576, V^T chunk p - 576 (dh row
+  // (p - 576) / 8, chunk position (p - 576) % 8 holding key chunk position ^ swz(row))
+  // below 1152, else nothing (the load reads zeros into the spare slot). Whole
+  // wavefronts fall in one part, since both parts are multiples of 64 chunks.
+  int goff[LPT];
+  bool isk[LPT], inr[LPT];
+#pragma unroll
+  for (int i = 0; i < LPT; ++i) {
+    const int p = i * 256 + tid;
+    isk[i] = p < kD72K;
+    inr[i] = p < NCH;
+    if (p < kD72K) {
+      goff[i] = p * 16;
+    } else if (p < NCH) {
+      const int pv = p - kD72K, row = pv / 8;
+      goff[i] = (row * a.ldv + (((pv % 8) ^ dma_swz<8>(row)) * 8)) * 2;
+    } else {
+      goff[i] = kOffOOB;
+    }
+  }
+  auto issue = [&](char* sb, int step) {
+    const int kv0 = step * 2 * kKH;
+    const __amdgpu_buffer_rsrc_t k_src =
+        buffer_rsrc(Kg + (size_t)kv0 * DH, (uint32_t)max(a.Nk - kv0, 0) * DH * 2);
+    const __amdgpu_buffer_rsrc_t v_src = buffer_rsrc(Vt + kv0, (uint32_t)max(DH * a.ldv - kv0, 0) * 2);
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      // the wavefront's part is uniform (the parts are whole wavefronts)
+      char* dst = inr[i] ? sb + (isk[i] ? (i * 256 + wave * 64) * 16 : V_OFF + (i * 256 + wave * 64 - kD72K) * 16)
+                         : g_attn72_spare;
+      buffer_load16_lds(isk[i] ? k_src : v_src, dst, goff[i]);
+    }
+  };
+
+  f32x16 o[QB][DB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[qb][b][e] = 0.0f;
+  float m2[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) m2[qb] = -INFINITY;
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const int sw = dma_swz<8>(l32);
+  const int krow = (kh * kKH + l32) * 9;
+
+  constexpr int kWait = waitcnt_vm_lgkm0<(kAttnStages - 2) * LPT>();
+  auto step = [&](auto s, int it) {
+    constexpr int S = decltype(s)::value;
+    __builtin_amdgcn_s_waitcnt(kWait);
+    bare_barrier();
+    issue(stage(std::integral_constant<int, S + kAttnStages - 1>{}), it + kAttnStages - 1);
+    const char* cur = stage(std::integral_constant<int, S>{});
+    const int kv0 = it * 2 * kKH + kh * kKH;
+    if (kv0 >= a.Nk) return;
+    f32x16 sc[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[qb][e] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < DHC; ++kk) {
+      bf16x8 kf = *(const bf16x8*)(cur + (krow + kk * 2 + g) * 16);
+      if (kk == DHC - 1 && g == 1) kf = bf16x8{};  // dh 72..79
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][kk], sc[qb], 0, 0, 0);
+    }
+    if (kv0 + kKH > a.Nk) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) sc[qb][e] = -INFINITY;
+    }
+    bf16x8 pf[QB][2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float tmax = sc[qb][0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[qb][e]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+      if (__any(tmax > m2[qb] + kLazy)) {
+        const float mnew = fmaxf(m2[qb], tmax);
+        const float alpha = __builtin_amdgcn_exp2f(m2[qb] - mnew);
+#pragma unroll
+        for (int b = 0; b < DB; ++b)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[qb][b][e] *= alpha;
+        m2[qb] = mnew;
+      }
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pf[qb][ks][j] = (bf16)__builtin_amdgcn_exp2f(fmaf(sc[qb][ks * 8 + j], sl2, -m2[qb]));
+    }
+#pragma unroll
+    for (int b = 0; b < DB; ++b) {
+      const char* vrow = cur + V_OFF + (b * 32 + l32) * 8 * 16;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x8 vf = *(const bf16x8*)(vrow + (((kh * 4 + 2 * ks + g) ^ sw) << 4));
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          o[qb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb][ks], o[qb][b], 0, 0, 0);
+      }
+    }
+  };
+
+  const int nsteps = (a.Nk + 2 * kKH - 1) / (2 * kKH);
+  // the constant rows are in place before any stage is read
+  __syncthreads();
+  issue(stage(std::integral_constant<int, 0>{}), 0);
+  issue(stage(std::integral_constant<int, 1>{}), 1);
+  int it = 0;
+  for (; it + kAttnStages <= nsteps; it += kAttnStages) {
+    step(std::integral_constant<int, 0>{}, it);
+    step(std::integral_constant<int, 1>{}, it + 1);
+    step(std::integral_constant<int, 2>{}, it + 2);
+  }
+  if (it < nsteps) step(std::integral_constant<int, 0>{}, it);
+  if (it + 1 < nsteps) step(std::integral_constant<int, 1>{}, it + 1);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  // the ones row's output (row kSumRow of the last block: register 12 of lane half 0;
+  // lane half 1 holds row kSumRow + 4, a zero row) is this wavefront's probability sum
+  float lsum[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) lsum[qb] = o[qb][DB - 1][12];
+  float* mg = (float*)(qg == 0 ? st0 : st1);
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    if (qb > 0) __syncthreads();  // the previous block's values were read
+    if (kh == 1) {
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mg[(b * 16 + e) * 64 + lane] = o[qb][b][e];
+      mg[DB * 16 * 64 + lane] = m2[qb];
+      mg[(DB * 16 + 1) * 64 + lane] = lsum[qb];
+    }
+    __syncthreads();
+    if (kh == 1) continue;
+    const float m2b = mg[DB * 16 * 64 + lane];
+    const float mnew = fmaxf(m2[qb], m2b);
+    const float a0 = m2[qb] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2[qb] - mnew);
+    const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
+    const bool own = m2[qb] != -INFINITY, other = m2b != -INFINITY;
+    float ls = (own ? lsum[qb] * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
+    ls += __shfl_xor(ls, 32);
+    const float inv = 1.0f / ls;
+    if (qi[qb] < a.Nq) {
+      bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi[qb]) * a.D + (size_t)head * DH;
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int d = b * 32 + e4 * 8 + g * 4;
+          float w[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int e = e4 * 4 + q;
+            w[q] = ((own ? o[qb][b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
+          }
+          if (d < DH) *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
+        }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ fp32
 constexpr int kFKV = 32;
 
@@ -816,7 +1071,12 @@ hipError_t launch_attention(bool use_bf16, const AttnArgs& args, hipStream_t s) 
         else
           launch_bf16_inst<4, 2>(a, two, s);
         break;
-      case 5: launch_bf16_inst<5, 3>(a, two, s); break;
+      case 5:
+        if (a.dh == 72 && two)
+          launch(attn_bf16_dma72x2_kernel, dim3(((a.Nq + kQB2 - 1) / kQB2) * a.heads * a.rows), dim3(256), 0, s, a);
+        else
+          launch_bf16_inst<5, 3>(a, two, s);
+        break;
       case 6: launch_bf16_inst<6, 3>(a, two, s); break;
       case 7: launch_bf16_inst<7, 4>(a, two, s); break;
       case 8: launch_bf16_inst<8, 4>(a, two, s); break;
