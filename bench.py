@@ -46,17 +46,17 @@ MI355X_HBM_GBS = 8000.0
 # only for the kernel sources it was measured on (hash below); otherwise traffic is null.
 KERNEL_SOURCES = ("k_gemm.hip", "k_attn.hip", "sf_device.h", "sf_launch.h")
 TRAFFIC = {
-    ("s512", "bf16", "FC2"): {"bytes": 94522405, "sources": "e634ccf7e5fca853",
+    ("s512", "bf16", "FC2"): {"bytes": 94516884, "sources": "88561669cb4e3b30",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512", "bf16", "FC1"): {"bytes": 59973659, "sources": "e634ccf7e5fca853",
+    ("s512", "bf16", "FC1"): {"bytes": 59971301, "sources": "88561669cb4e3b30",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512_large", "bf16", "FC2"): {"bytes": 185915855, "sources": "e634ccf7e5fca853",
+    ("s512_large", "bf16", "FC2"): {"bytes": 185630864, "sources": "88561669cb4e3b30",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_large", "bf16", "FC1"): {"bytes": 132230923, "sources": "e634ccf7e5fca853",
+    ("s512_large", "bf16", "FC1"): {"bytes": 132287964, "sources": "88561669cb4e3b30",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_cfg", "bf16", "FC2"): {"bytes": 381436650, "sources": "e634ccf7e5fca853",
+    ("s512_cfg", "bf16", "FC2"): {"bytes": 383832290, "sources": "88561669cb4e3b30",
                                   "profile": "profiles/stream_step_s512_cfg_bf16.md"},
-    ("s1024", "bf16", "ATTN"): {"bytes": 161664252, "sources": "e634ccf7e5fca853",
+    ("s1024", "bf16", "ATTN"): {"bytes": 161357402, "sources": "88561669cb4e3b30",
                                 "profile": "profiles/stream_step_s1024_bf16.md"},
 }
 
