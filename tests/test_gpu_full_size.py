@@ -100,16 +100,21 @@ def test_s512_eight_rows_equal_each_row_alone():
 def test_dh72_staged_two_block_attention_equals_each_row_alone():
     """Head dim 72 with at least 512 workgroups of 128 queries runs the directly staged
     two-block attention kernel; one row alone runs the register-staged one-block kernel.
-    The 512^2 width-1152 network over 4 rows (512 workgroups), and a one-block 300-token
-    network of the same width (ragged query and key blocks) over 12 rows (576), against
-    each row alone: the same bits."""
+    The 512^2 width-1152 network over 4 rows (512 workgroups), a one-block 300-token
+    network of the same width (ragged query and key blocks) over 12 rows (576), and a
+    16-token one over 32 rows (512, the second key half of every workgroup empty),
+    against each row alone: the same bits."""
     from dataclasses import replace
 
     from paper_2511_22009_amd import Model, Precision
     big = W.get_config("s512_large")
     short = replace(big, name="dh72_300tok", H=20, W=60, L=1)
     m_short = Model(W.make_blob(short), Precision.BF16, 12)
-    for cfg, m, B in ((big, model("s512_large", "bf16", max_rows=big.rows), 4), (short, m_short, 12)):
+    # 16 tokens: every key in the first key half, the second half of each workgroup empty
+    tiny = replace(big, name="dh72_16tok", H=8, W=8, L=1)
+    m_tiny = Model(W.make_blob(tiny), Precision.BF16, 32)
+    for cfg, m, B in ((big, model("s512_large", "bf16", max_rows=big.rows), 4), (short, m_short, 12),
+                      (tiny, m_tiny, 32)):
         x = W.latents(cfg, B, seed=90 + B)
         t = np.random.default_rng(91 + B).uniform(0.0, 1.0, B).astype(np.float32)
         full = host(m.velocity(dev(x), t))
