@@ -202,7 +202,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         float tmax = s[qb][0];
 #pragma unroll
         for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, s[qb][e]);
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+        tmax = pair32_max(tmax) * sl2;
         if (__any(tmax > m2[qb] + kLazy)) {
           const float mnew = fmaxf(m2[qb], tmax);
           const float alpha = __builtin_amdgcn_exp2f(m2[qb] - mnew);
@@ -270,7 +270,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     // not multiplied by a zero weight
     const bool own = m2[qb] != -INFINITY, other = m2b != -INFINITY;
     float ls = (own ? lsum[qb] * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
-    ls += __shfl_xor(ls, 32);
+    ls = pair32_sum(ls);
     const float inv = 1.0f / ls;
     if (qi[qb] < a.Nq) {
       bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi[qb]) * a.D + (size_t)head * dh;
@@ -408,7 +408,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
     float tmax = sc[0];
 #pragma unroll
     for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[e]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+    tmax = pair32_max(tmax) * sl2;
     if (__any(tmax > m2 + kLazy)) {
       const float mnew = fmaxf(m2, tmax);
       const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
@@ -479,7 +479,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   // not multiplied by a zero weight
   const bool own = m2 != -INFINITY, other = m2b != -INFINITY;
   lsum = (own ? lsum * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
-  lsum += __shfl_xor(lsum, 32);
+  lsum = pair32_sum(lsum);
   const float inv = 1.0f / lsum;
   if (qi < a.Nq) {
     bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi) * a.D + (size_t)head * DH;
@@ -622,7 +622,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
       float tmax = sc[qb][0];
 #pragma unroll
       for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[qb][e]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+      tmax = pair32_max(tmax) * sl2;
       if (__any(tmax > m2[qb] + kLazy)) {
         const float mnew = fmaxf(m2[qb], tmax);
         const float alpha = __builtin_amdgcn_exp2f(m2[qb] - mnew);
@@ -692,7 +692,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
       const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
       const bool own = m2[qb] != -INFINITY, other = m2b != -INFINITY;
       float ls = (own ? lsum[qb] * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
-      ls += __shfl_xor(ls, 32);
+      ls = pair32_sum(ls);
       const float inv = 1.0f / ls;
       if (qi[qb] < a.Nq) {
         bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi[qb]) * a.D + (size_t)head * DH;
@@ -879,7 +879,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
       float tmax = sc[qb][0];
 #pragma unroll
       for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[qb][e]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * sl2;
+      tmax = pair32_max(tmax) * sl2;
       if (__any(tmax > m2[qb] + kLazy)) {
         const float mnew = fmaxf(m2[qb], tmax);
         const float alpha = __builtin_amdgcn_exp2f(m2[qb] - mnew);
@@ -948,7 +948,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
     const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
     const bool own = m2[qb] != -INFINITY, other = m2b != -INFINITY;
     float ls = (own ? lsum[qb] * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
-    ls += __shfl_xor(ls, 32);
+    ls = pair32_sum(ls);
     const float inv = 1.0f / ls;
     if (qi[qb] < a.Nq) {
       bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi[qb]) * a.D + (size_t)head * DH;

@@ -31,6 +31,22 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Max and sum of v over the lane pair (l, l ^ 32), in vector registers.
+// v_permlane32_swap with v as both operands returns (r0, r1) where lane l < 32 holds
+// (v[l], v[l + 32]) and lane l >= 32 holds (v[l - 32], v[l]). So max(r0, r1) and r0 + r1
+// are the pair's max and sum in every lane. Both operations commute, so the bits equal
+// those of v op __shfl_xor(v, 32), which goes through the LDS crossbar (ds_bpermute)
+// and waits behind any LDS traffic.
+__device__ __forceinline__ float pair32_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float pair32_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Sums each of 16 per-lane values over the 64 lanes of a wavefront and returns, in
 // lane l, the total of index (l >> 2) & 15 (lanes 4i..4i+3 all hold total i). Butterfly
 // reduce-scatter: four halving exchanges (xor 32, 16, 8, 4; 8 + 4 + 2 + 1 shuffles) then
