@@ -395,11 +395,15 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
     f32x16 sc;
 #pragma unroll
     for (int e = 0; e < 16; ++e) sc[e] = 0.0f;
+    // all K fragments are read before the first MFMA, so their LDS latencies overlap
+    // (the compiler otherwise waits for each pair in turn)
+    bf16x8 kf[DHC];
 #pragma unroll
-    for (int kk = 0; kk < DHC; ++kk) {
-      const bf16x8 kf = *(const bf16x8*)(cur + (krow + ((kk * 2 + g) ^ sw)) * 16);
-      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sc, 0, 0, 0);
-    }
+    for (int kk = 0; kk < DHC; ++kk) kf[kk] = *(const bf16x8*)(cur + (krow + ((kk * 2 + g) ^ sw)) * 16);
+#pragma unroll
+    for (int kk = 0; kk < DHC; ++kk) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sc, 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, DHC, 0);  // LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, DHC, 0);  // then the MFMAs
     if (kv0 + kKH > a.Nk) {
 #pragma unroll
       for (int e = 0; e < 16; ++e)
@@ -603,12 +607,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[qb][e] = 0.0f;
+    bf16x8 kf[DHC];
 #pragma unroll
-    for (int kk = 0; kk < DHC; ++kk) {
-      const bf16x8 kf = *(const bf16x8*)(cur + (krow + ((kk * 2 + g) ^ sw)) * 16);
+    for (int kk = 0; kk < DHC; ++kk) kf[kk] = *(const bf16x8*)(cur + (krow + ((kk * 2 + g) ^ sw)) * 16);
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][kk], sc[qb], 0, 0, 0);
-    }
+    for (int kk = 0; kk < DHC; ++kk)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[qb][kk], sc[qb], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, DHC, 0);       // LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, DHC * QB, 0);  // then the MFMAs
     if (kv0 + kKH > a.Nk) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
@@ -859,13 +866,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[qb][e] = 0.0f;
+    bf16x8 kf[DHC];
 #pragma unroll
-    for (int kk = 0; kk < DHC; ++kk) {
-      bf16x8 kf = *(const bf16x8*)(cur + (krow + kk * 2 + g) * 16);
-      if (kk == DHC - 1 && g == 1) kf = bf16x8{};  // dh 72..79
+    for (int kk = 0; kk < DHC; ++kk) kf[kk] = *(const bf16x8*)(cur + (krow + kk * 2 + g) * 16);
+    if (g == 1) kf[DHC - 1] = bf16x8{};  // dh 72..79
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][kk], sc[qb], 0, 0, 0);
-    }
+    for (int kk = 0; kk < DHC; ++kk)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[qb][kk], sc[qb], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, DHC, 0);       // LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, DHC * QB, 0);  // then the MFMAs
     if (kv0 + kKH > a.Nk) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
