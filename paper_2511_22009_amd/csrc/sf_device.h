@@ -19,15 +19,58 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
   return (uint32_t)(((uint64_t)__umulhi(n, f.magic) + n) >> f.shift);
 }
 
+// The value that lane l ^ M holds, moved in vector registers without the LDS crossbar
+// that __shfl_xor (ds_bpermute) goes through, where each exchange waits a full LDS round
+// trip, behind any other LDS traffic of the CU:
+//   M = 1, 2: DPP quad_perm [1,0,3,2] and [2,3,0,1];
+//   M = 4: DPP row_shl:4 written to lanes 0-3 and 8-11 of each 16-lane row (bank mask
+//          0101), then row_shr:4 to lanes 4-7 and 12-15 (bank mask 1010);
+//   M = 8: DPP row_ror:8 (rotation by 8 within a 16-lane row);
+//   M = 16, 32: v_permlane16_swap / v_permlane32_swap with v as both operands, which
+//          return (r0, r1) with r1 = v[l + M] in the lanes whose bit M is clear and
+//          r0 = v[l - M] in the others.
+// (Lane layouts of all six checked on the GPU against l ^ M.)
+template <int M>
+__device__ __forceinline__ float lane_xor(float v) {
+  const int x = __float_as_int(v);
+  if constexpr (M == 1) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, true));
+  } else if constexpr (M == 2) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, true));
+  } else if constexpr (M == 4) {
+    const int y = __builtin_amdgcn_update_dpp(x, x, 0x104, 0xF, 0x5, false);
+    return __int_as_float(__builtin_amdgcn_update_dpp(y, x, 0x114, 0xF, 0xA, false));
+  } else if constexpr (M == 8) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, true));
+  } else if constexpr (M == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap((unsigned)x, (unsigned)x, false, false);
+    return __uint_as_float((threadIdx.x & 16) ? r[0] : r[1]);
+  } else {
+    static_assert(M == 32, "lane_xor: M is 1, 2, 4, 8, 16 or 32");
+    const auto r = __builtin_amdgcn_permlane32_swap((unsigned)x, (unsigned)x, false, false);
+    return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+  }
+}
+
+// Butterfly over lane xor 32, 16, 8, 4, 2, 1 (each lane adds its partner's value to
+// its own, so every lane ends with the same bits).
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  v += lane_xor<32>(v);
+  v += lane_xor<16>(v);
+  v += lane_xor<8>(v);
+  v += lane_xor<4>(v);
+  v += lane_xor<2>(v);
+  v += lane_xor<1>(v);
   return v;
 }
 
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  v = fmaxf(v, lane_xor<32>(v));
+  v = fmaxf(v, lane_xor<16>(v));
+  v = fmaxf(v, lane_xor<8>(v));
+  v = fmaxf(v, lane_xor<4>(v));
+  v = fmaxf(v, lane_xor<2>(v));
+  v = fmaxf(v, lane_xor<1>(v));
   return v;
 }
 
@@ -49,8 +92,12 @@ __device__ __forceinline__ float pair32_sum(float v) {
 
 // Sums each of 16 per-lane values over the 64 lanes of a wavefront and returns, in
 // lane l, the total of index (l >> 2) & 15 (lanes 4i..4i+3 all hold total i). Butterfly
-// reduce-scatter: four halving exchanges (xor 32, 16, 8, 4; 8 + 4 + 2 + 1 shuffles) then
-// two plain ones (xor 2, 1): 17 shuffles instead of 16 separate 6-step reductions.
+// reduce-scatter: four halving exchanges (lane xor 32, 16, 8, 4) then two plain ones
+// (xor 2, 1). In a halving exchange over bit M a lane keeps half of its values ("mine")
+// and receives its partner's copy of that half. For M = 32 and 16 one lane swap moves
+// both halves at once: with X = the lower half and Y = the upper half as operands, a
+// lane whose bit M is clear reads its partner's X in r1, the others their partner's Y
+// in r0.
 __device__ __forceinline__ float wave_reduce16(float (&v)[16]) {
   const int lane = threadIdx.x & 63;
   float a8[8], a4[4], a2[2];
@@ -58,18 +105,16 @@ __device__ __forceinline__ float wave_reduce16(float (&v)[16]) {
     const bool hi = lane & 32;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const float mine = hi ? v[8 + i] : v[i];
-      const float give = hi ? v[i] : v[8 + i];
-      a8[i] = mine + __shfl_xor(give, 32);
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]), __float_as_uint(v[8 + i]), false, false);
+      a8[i] = hi ? v[8 + i] + __uint_as_float(r[0]) : v[i] + __uint_as_float(r[1]);
     }
   }
   {
     const bool hi = lane & 16;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float mine = hi ? a8[4 + i] : a8[i];
-      const float give = hi ? a8[i] : a8[4 + i];
-      a4[i] = mine + __shfl_xor(give, 16);
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a8[i]), __float_as_uint(a8[4 + i]), false, false);
+      a4[i] = hi ? a8[4 + i] + __uint_as_float(r[0]) : a8[i] + __uint_as_float(r[1]);
     }
   }
   {
@@ -78,13 +123,13 @@ __device__ __forceinline__ float wave_reduce16(float (&v)[16]) {
     for (int i = 0; i < 2; ++i) {
       const float mine = hi ? a4[2 + i] : a4[i];
       const float give = hi ? a4[i] : a4[2 + i];
-      a2[i] = mine + __shfl_xor(give, 8);
+      a2[i] = mine + lane_xor<8>(give);
     }
   }
   const bool hi = lane & 4;
-  float r = (hi ? a2[1] : a2[0]) + __shfl_xor(hi ? a2[0] : a2[1], 4);
-  r += __shfl_xor(r, 2);
-  r += __shfl_xor(r, 1);
+  float r = (hi ? a2[1] : a2[0]) + lane_xor<4>(hi ? a2[0] : a2[1]);
+  r += lane_xor<2>(r);
+  r += lane_xor<1>(r);
   return r;
 }
 
