@@ -166,7 +166,9 @@ hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s) {
 // output columns in registers for all of the workgroup's tokens, so the weight is read
 // once per kEmbedWgTok tokens (not once per four, as with a thread per four tokens:
 // 8.8 -> 6.5 us at 4096 tokens x 768, 41.8 -> 24.0 us at 16384 x 1152, same bits).
-// All of a thread's position-row loads are issued before its first token is computed.
+// All of a thread's weight, bias and position-row loads for its first column group are
+// issued before the patch values are staged, so the two memory latencies overlap
+// instead of following each other across the barrier.
 constexpr int kEmbedWgTok = 8;
 
 __global__ __launch_bounds__(256) void embed_p2c4_kernel(EmbedArgs a) {
@@ -175,33 +177,27 @@ __global__ __launch_bounds__(256) void embed_p2c4_kernel(EmbedArgs a) {
   const int m0 = blockIdx.x * kEmbedWgTok;
   const int tid = threadIdx.x;
   const int gwn = a.W / 2;
-  if (tid < kEmbedWgTok * 8) {
-    const int t = tid >> 3, c = (tid >> 1) & 3, i = tid & 1;
-    const int m = min(m0 + t, M - 1);
-    const int r = m / a.N, n = m - r * a.N;
-    const int lat = r % a.n_lat;
-    const int gh = n / gwn, gw = n - gh * gwn;
-    const float2 v = *(const float2*)(a.x + (((size_t)lat * 4 + c) * a.H + gh * 2 + i) * a.W + gw * 2);
-    float* ps = (float*)&px_s[t][0];
-    ps[(2 * i + 0) * 4 + c] = v.x;
-    ps[(2 * i + 1) * 4 + c] = v.y;
-  }
-  __syncthreads();
   const int d4n = a.D >> 2;
   const int nt = min(kEmbedWgTok, M - m0);
-  for (int c4 = tid; c4 < d4n; c4 += 256) {
-    const int d = 4 * c4;
-    float4 w[16];
+  struct Cols {
+    float4 w[16], b, pos[kEmbedWgTok];
+  };
+  // loads of column group c4 (clamped to an in-bounds group; its results are used only
+  // if c4 < d4n)
+  auto load_cols = [&](int c4, Cols& k) {
+    const int d = 4 * min(c4, d4n - 1);
 #pragma unroll
-    for (int f = 0; f < 16; ++f) w[f] = *(const float4*)(a.W_pe + (size_t)f * a.D + d);
-    const float4 b = *(const float4*)(a.b_pe + d);
-    float4 pos[kEmbedWgTok];
+    for (int f = 0; f < 16; ++f) k.w[f] = *(const float4*)(a.W_pe + (size_t)f * a.D + d);
+    k.b = *(const float4*)(a.b_pe + d);
 #pragma unroll
     for (int t = 0; t < kEmbedWgTok; ++t) {
       const int m = min(m0 + t, M - 1);
       const int n = m - (m / a.N) * a.N;
-      pos[t] = *(const float4*)(a.pos + (size_t)n * a.D + d);
+      k.pos[t] = *(const float4*)(a.pos + (size_t)n * a.D + d);
     }
+  };
+  auto compute_cols = [&](int c4, const Cols& k) {
+    const int d = 4 * c4;
 #pragma unroll
     for (int t = 0; t < kEmbedWgTok; ++t) {
       if (t >= nt) break;
@@ -212,14 +208,41 @@ __global__ __launch_bounds__(256) void embed_p2c4_kernel(EmbedArgs a) {
         const float p4[4] = {pv.x, pv.y, pv.z, pv.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float4 wf = w[4 * q + e];
+          const float4 wf = k.w[4 * q + e];
           acc.x += p4[e] * wf.x; acc.y += p4[e] * wf.y; acc.z += p4[e] * wf.z; acc.w += p4[e] * wf.w;
         }
       }
       *(float4*)(a.h + (size_t)(m0 + t) * a.D + d) =
-          make_float4((acc.x + b.x) + pos[t].x, (acc.y + b.y) + pos[t].y, (acc.z + b.z) + pos[t].z,
-                      (acc.w + b.w) + pos[t].w);
+          make_float4((acc.x + k.b.x) + k.pos[t].x, (acc.y + k.b.y) + k.pos[t].y, (acc.z + k.b.z) + k.pos[t].z,
+                      (acc.w + k.b.w) + k.pos[t].w);
     }
+  };
+  // the patch-value load first, so that staging it waits for it alone
+  const bool stager = tid < kEmbedWgTok * 8;
+  const int st = tid >> 3, sc = (tid >> 1) & 3, si = tid & 1;
+  float2 pxv;
+  {
+    const int m = min(m0 + st, M - 1);
+    const int r = m / a.N, n = m - r * a.N;
+    const int lat = r % a.n_lat;
+    const int gh = n / gwn, gw = n - gh * gwn;
+    // threads past the stagers load the first stager's value (in bounds, unused)
+    pxv = *(const float2*)(a.x + (((size_t)lat * 4 + (stager ? sc : 0)) * a.H + gh * 2 + (stager ? si : 0)) * a.W + gw * 2);
+  }
+  __builtin_amdgcn_sched_barrier(0);  // keep it ahead of the column loads
+  Cols first;
+  load_cols(tid, first);
+  if (stager) {
+    float* ps = (float*)&px_s[st][0];
+    ps[(2 * si + 0) * 4 + sc] = pxv.x;
+    ps[(2 * si + 1) * 4 + sc] = pxv.y;
+  }
+  __syncthreads();
+  if (tid < d4n) compute_cols(tid, first);
+  for (int c4 = tid + 256; c4 < d4n; c4 += 256) {
+    Cols k;
+    load_cols(c4, k);
+    compute_cols(c4, k);
   }
 }
 

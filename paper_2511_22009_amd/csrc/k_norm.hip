@@ -24,7 +24,12 @@ template <> struct Store4<bf16> {
 
 // RPW rows per wavefront, NV float4 per lane per row (D <= 256 NV). Every load of
 // the wavefront's rows and of their table entries (shift and scale) is issued before
-// the first reduction, so the kernel pays one memory latency per row group.
+// the first reduction, so the kernel pays one memory latency per row group. The loads
+// are unconditional, at in-bounds indices (chunk 0 stands in for chunks past the row's
+// end; a plain LN reads its unused shift and scale from the row itself), and the zeros
+// of the chunks past the end are selected once all loads are issued: a load under a
+// lane condition makes the compiler wait for it before the other path writes the same
+// registers, which would cost one memory latency per chunk.
 template <typename OT, int NV, int RPW>
 __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
   const int lane = threadIdx.x & 63;
@@ -36,8 +41,8 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
   for (int r = 0; r < RPW; ++r) {
     const int m = min(mb + r, a.M - 1);
     const float4* row = (const float4*)(a.h + (size_t)m * a.D);
-    const float* tsh = nullptr;
-    const float* tsc = nullptr;
+    const float* tsh = (const float*)row;
+    const float* tsc = (const float*)row;
     if (a.table) {
       const int q = (int)fdiv((uint32_t)m, a.tok);
       const int slot = q < a.n_slots ? q : q - a.n_slots;
@@ -47,17 +52,17 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int c = lane + i * 64;
-      const bool in = c < nv;
-      v[r][i] = in ? row[c] : make_float4(0.f, 0.f, 0.f, 0.f);
-      if (a.table && in) {
-        sc[r][i] = *(const float4*)(tsc + 4 * c);
-        sh[r][i] = *(const float4*)(tsh + 4 * c);
-      } else {
-        sc[r][i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        sh[r][i] = make_float4(0.f, 0.f, 0.f, 0.f);
-      }
+      const int cc = c < nv ? c : 0;
+      v[r][i] = row[cc];
+      sc[r][i] = *(const float4*)(tsc + 4 * cc);
+      sh[r][i] = *(const float4*)(tsh + 4 * cc);
     }
   }
+#pragma unroll
+  for (int r = 0; r < RPW; ++r)
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (lane + i * 64 >= nv) v[r][i] = make_float4(0.f, 0.f, 0.f, 0.f);
   float mean[RPW], rstd[RPW];
 #pragma unroll
   for (int r = 0; r < RPW; ++r) {
@@ -158,14 +163,19 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
       const float* tsc = a.table + (size_t)slot * a.ldt + a.scale_off;
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
+        // unconditional loads at in-bounds indices, zeros selected after all are issued
         const int c = lane + i * 64;
-        const bool in = c < nv;
-        const int cc = in ? c : 0;
-        v[r][i] = in ? row[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+        const int cc = c < nv ? c : 0;
+        v[r][i] = row[cc];
         sc[r][i] = *(const float4*)(tsc + 4 * cc);
         sh[r][i] = *(const float4*)(tsh + 4 * cc);
       }
     }
+#pragma unroll
+    for (int r = 0; r < RH; ++r)
+#pragma unroll
+      for (int i = 0; i < NV; ++i)
+        if (lane + i * 64 >= nv) v[r][i] = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int r = 0; r < RH; ++r) {
       float s = 0.0f;
