@@ -441,7 +441,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
   constexpr int SPARE = 2 * (BM + BN) * LDK;  // bf16 index of the spare slot
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   // wavefront (kg, wm, wn): sub-tile (wm, wn) over K quarter-slices kg*KS .. kg*KS+KS-1
   // of every 64-wide K slice
   const int kg = wave / (WM * WN), wmn = wave - kg * (WM * WN);
@@ -484,8 +484,25 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
     b_off[i] = (in && n0 + row < a.N) ? ((n0 + row) * a.ldb + b_kc[i]) * 2 : kOffOOB;
   }
   u32x4 ra[ACH], rb[BCH];
-  auto gload = [&](int kt) {
+  // FAST (K a multiple of BK): every slice lies wholly inside K or wholly past it, so
+  // the loads go through resources based at the slice's first column and each thread's
+  // offsets are the fixed ones of k = 0 (rows past M keep the out-of-range offset); a
+  // slice past K gets empty resources and reads zeros. The main loop is compiled once
+  // per form and chosen by K, so neither carries a per-slice branch.
+  auto gload = [&](auto fastc, int kt) {
     const int k0 = kt * BK;
+    if constexpr (decltype(fastc)::value) {
+      const bool live = k0 < a.K;
+      const __amdgpu_buffer_rsrc_t ra1 =
+          buffer_rsrc((const char*)a.A + 2 * (size_t)k0, live ? (uint32_t)a.M * a.lda * 2 - 2 * k0 : 0u);
+      const __amdgpu_buffer_rsrc_t rb1 =
+          buffer_rsrc((const char*)a.B + 2 * (size_t)k0, live ? (uint32_t)a.N * a.ldb * 2 - 2 * k0 : 0u);
+#pragma unroll
+      for (int i = 0; i < ACH; ++i) ra[i] = buffer_load16(ra1, a_off[i]);
+#pragma unroll
+      for (int i = 0; i < BCH; ++i) rb[i] = buffer_load16(rb1, b_off[i]);
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < ACH; ++i)
       ra[i] = buffer_load16(ra_src, (k0 + a_kc[i] < a.K && a_off[i] != kOffOOB) ? a_off[i] + 2 * k0 : kOffOOB);
@@ -514,7 +531,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  auto step = [&](int cur, int kt, bool write_next, bool load_next) {
+  auto step = [&](auto fastc, int cur, int kt, bool write_next, bool load_next) {
     const bf16* Ab = As + cur * BM * LDK + (wm * TM * 32 + l32) * LDK + g * 8 + kg * KS * 16;
     const bf16* Bb = Bs + cur * BN * LDK + (wn * TN * 32 + l32) * LDK + g * 8 + kg * KS * 16;
     bf16x8 af[2][TM], bfr[2][TN];
@@ -538,7 +555,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cb][j], af[cb][i], acc[i][j], 0, 0, 0);
     }
     if (write_next) lstore(cur ^ 1);
-    if (load_next) gload(kt + 2);
+    if (load_next) gload(fastc, kt + 2);
     // interleave: the fragment reads ahead of their MFMAs over the first half of the
     // MFMAs, the LDS writes and global loads over the second half
     constexpr int H1 = NMFMA / 2, H2 = NMFMA - NMFMA / 2;
@@ -556,22 +573,28 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
   };
 
   const int nk = (a.K + BK - 1) / BK;
-  gload(0);
-  lstore(0);
-  if (nk > 1) gload(1);
-  __syncthreads();
-  int kt = 0;
-  for (; kt + 2 < nk; ++kt) {
-    step(kt & 1, kt, true, true);
+  auto main_loop = [&](auto fastc) {
+    gload(fastc, 0);
+    lstore(0);
+    if (nk > 1) gload(fastc, 1);
     __syncthreads();
-  }
-  if (kt + 1 < nk) {
-    step(kt & 1, kt, true, false);
+    int kt = 0;
+    for (; kt + 2 < nk; ++kt) {
+      step(fastc, kt & 1, kt, true, true);
+      __syncthreads();
+    }
+    if (kt + 1 < nk) {
+      step(fastc, kt & 1, kt, true, false);
+      __syncthreads();
+      ++kt;
+    }
+    step(fastc, kt & 1, kt, false, false);
     __syncthreads();
-    ++kt;
-  }
-  step(kt & 1, kt, false, false);
-  __syncthreads();
+  };
+  if (a.K % BK == 0)
+    main_loop(std::true_type{});
+  else
+    main_loop(std::false_type{});
 
   // The MFMAs compute C^T blocks (weights as the first operand), so in acc[i][j]
   // lane (l32, g) holds row (wm*TM + i)*32 + l32 of the tile and, in registers
@@ -692,7 +715,9 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   };
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  // the wavefront index is uniform: kept scalar, so the LDS destinations of the direct
+  // loads (M0) need no readfirstlane
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kg = wave / (WM * WN), wmn = wave - kg * (WM * WN);
   const int wm = wmn / WN, wn = wmn % WN;
   const int l32 = lane & 31, g = lane >> 5;
@@ -728,8 +753,30 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   }
   // slice kt into stage buffer sb: every thread issues exactly LPT loads (past the end
   // of K they read zeros), each wavefront's 64 lanes filling one contiguous kilobyte
-  auto issue = [&](char* sb, int kt) {
+  // FAST (K a multiple of BK): every slice lies wholly inside K or wholly past it, so
+  // the loads go through resources based at the slice's first column and each thread's
+  // offsets are the fixed ones of k = 0 (rows past M keep the out-of-range offset); a
+  // slice past K gets empty resources and reads zeros without touching memory
+  auto issue = [&](auto fast, char* sb, int kt) {
     const int k0 = kt * BK;
+    if constexpr (decltype(fast)::value) {
+      const bool live = k0 < a.K;
+      const __amdgpu_buffer_rsrc_t ra =
+          buffer_rsrc((const char*)a.A + 2 * (size_t)k0, live ? (uint32_t)a.M * a.lda * 2 - 2 * k0 : 0u);
+      const __amdgpu_buffer_rsrc_t rb =
+          buffer_rsrc((const char*)a.B + 2 * (size_t)k0, live ? (uint32_t)a.N * a.ldb * 2 - 2 * k0 : 0u);
+#pragma unroll
+      for (int i = 0; i < ACH; ++i) {
+        const bool in = ATOT % NT == 0 || i * NT + wave * 64 < ATOT;
+        buffer_load16_lds(ra, in ? sb + (i * NT + wave * 64) * 16 : spare, a_off[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < BCH; ++i) {
+        const bool in = BTOT % NT == 0 || i * NT + wave * 64 < BTOT;
+        buffer_load16_lds(rb, in ? sb + ATOT * 16 + (i * NT + wave * 64) * 16 : spare, b_off[i]);
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
       const bool in = ATOT % NT == 0 || i * NT + wave * 64 < ATOT;
@@ -763,7 +810,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   // interleaved with the fragment reads and with the loads of slice kt + STAGES - 1
   // into the stage read in the previous step
   constexpr int kWait = waitcnt_vm_lgkm0<(STAGES - 2) * LPT>();
-  auto step = [&](auto s, int kt) {
+  auto step = [&](auto fast, auto s, int kt) {
     constexpr int S = decltype(s)::value;
     __builtin_amdgcn_s_waitcnt(kWait);
     bare_barrier();
@@ -791,7 +838,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cb][j], af[cb][i], acc[i][j], 0, 0, 0);
     }
-    issue(stage(std::integral_constant<int, S + STAGES - 1>{}), kt + STAGES - 1);
+    issue(fast, stage(std::integral_constant<int, S + STAGES - 1>{}), kt + STAGES - 1);
     constexpr int H1 = NMFMA / 2, H2 = NMFMA - NMFMA / 2;
 #pragma unroll
     for (int i = 0; i < H1; ++i) {
@@ -806,23 +853,29 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   };
 
   const int nk = (a.K + BK - 1) / BK;
-  issue(stage(std::integral_constant<int, 0>{}), 0);
-  issue(stage(std::integral_constant<int, 1>{}), 1);
-  if constexpr (STAGES > 3) issue(stage(std::integral_constant<int, 2>{}), 2);
-  // whole rounds of STAGES steps in a loop with one exit (early exits inside the round
-  // would give the loop header a path on which the stage it reads was just issued),
-  // then the remaining steps
-  int kt = 0;
-  for (; kt + STAGES <= nk; kt += STAGES) {
-    step(std::integral_constant<int, 0>{}, kt);
-    step(std::integral_constant<int, 1>{}, kt + 1);
-    step(std::integral_constant<int, 2>{}, kt + 2);
-    if constexpr (STAGES > 3) step(std::integral_constant<int, 3>{}, kt + 3);
-  }
-  if (kt < nk) step(std::integral_constant<int, 0>{}, kt);
-  if (kt + 1 < nk) step(std::integral_constant<int, 1>{}, kt + 1);
-  if constexpr (STAGES > 3)
-    if (kt + 2 < nk) step(std::integral_constant<int, 2>{}, kt + 2);
+  auto main_loop = [&](auto fast) {
+    issue(fast, stage(std::integral_constant<int, 0>{}), 0);
+    issue(fast, stage(std::integral_constant<int, 1>{}), 1);
+    if constexpr (STAGES > 3) issue(fast, stage(std::integral_constant<int, 2>{}), 2);
+    // whole rounds of STAGES steps in a loop with one exit (early exits inside the round
+    // would give the loop header a path on which the stage it reads was just issued),
+    // then the remaining steps
+    int kt = 0;
+    for (; kt + STAGES <= nk; kt += STAGES) {
+      step(fast, std::integral_constant<int, 0>{}, kt);
+      step(fast, std::integral_constant<int, 1>{}, kt + 1);
+      step(fast, std::integral_constant<int, 2>{}, kt + 2);
+      if constexpr (STAGES > 3) step(fast, std::integral_constant<int, 3>{}, kt + 3);
+    }
+    if (kt < nk) step(fast, std::integral_constant<int, 0>{}, kt);
+    if (kt + 1 < nk) step(fast, std::integral_constant<int, 1>{}, kt + 1);
+    if constexpr (STAGES > 3)
+      if (kt + 2 < nk) step(fast, std::integral_constant<int, 2>{}, kt + 2);
+  };
+  if (a.K % BK == 0)
+    main_loop(std::true_type{});
+  else
+    main_loop(std::false_type{});
   // the zero-filling loads past K land before the buffers are reused
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
