@@ -46,17 +46,17 @@ MI355X_HBM_GBS = 8000.0
 # only for the kernel sources it was measured on (hash below); otherwise traffic is null.
 KERNEL_SOURCES = ("k_gemm.hip", "k_attn.hip", "sf_device.h", "sf_launch.h")
 TRAFFIC = {
-    ("s512", "bf16", "FC2"): {"bytes": 94516884, "sources": "88561669cb4e3b30",
+    ("s512", "bf16", "FC2"): {"bytes": 94525009, "sources": "3ba7cf6f59b418bb",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512", "bf16", "FC1"): {"bytes": 59971301, "sources": "88561669cb4e3b30",
+    ("s512", "bf16", "FC1"): {"bytes": 59991757, "sources": "3ba7cf6f59b418bb",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512_large", "bf16", "FC2"): {"bytes": 185630864, "sources": "88561669cb4e3b30",
+    ("s512_large", "bf16", "FC2"): {"bytes": 187429980, "sources": "3ba7cf6f59b418bb",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_large", "bf16", "FC1"): {"bytes": 132287964, "sources": "88561669cb4e3b30",
+    ("s512_large", "bf16", "FC1"): {"bytes": 133715143, "sources": "3ba7cf6f59b418bb",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_cfg", "bf16", "FC2"): {"bytes": 383832290, "sources": "88561669cb4e3b30",
+    ("s512_cfg", "bf16", "FC2"): {"bytes": 383249474, "sources": "3ba7cf6f59b418bb",
                                   "profile": "profiles/stream_step_s512_cfg_bf16.md"},
-    ("s1024", "bf16", "ATTN"): {"bytes": 161357402, "sources": "88561669cb4e3b30",
+    ("s1024", "bf16", "ATTN"): {"bytes": 161856290, "sources": "3ba7cf6f59b418bb",
                                 "profile": "profiles/stream_step_s1024_bf16.md"},
 }
 
