@@ -363,6 +363,27 @@ def test_max_rows_velocity_parity(name, prec):
     assert max(errs) <= TOL[prec], max(errs)
 
 
+def test_gemm_k_not_multiple_of_slice_velocity_parity():
+    """Width 96 (2 heads of 48, MLP 384): the QKV projection (N 288), the attention output
+    projection (N 96) and fc1 (N 384) run the directly staged narrow GEMM with K = 96,
+    which is not a multiple of its 64-wide K slice, so every slice's operand loads take
+    the per-column K check (with K a multiple of 64 they go through resources rebased at
+    each slice instead). bf16 velocity of every slot against the oracle, and each row
+    alone against the batch, bit for bit."""
+    from paper_2511_22009_amd import Model, Precision
+    cfg = W.Config("w96", C=4, H=16, W=20, p=2, D=96, L=2, heads=2, mlp=384)
+    blob = W.make_blob(cfg)
+    x = W.latents(cfg, cfg.K)
+    t, _ = W.slot_times(cfg)
+    m = Model(blob, Precision.BF16, cfg.K)
+    got = host(m.velocity(dev(x), t))
+    ref = oracle.velocity(oracle.load_blob(blob), x, t)
+    errs = [rel_l2(got[k], ref[k]) for k in range(cfg.K)]
+    assert max(errs) <= TOL_BF16, errs
+    for k in range(cfg.K):
+        np.testing.assert_array_equal(got[k], host(m.velocity(dev(x[k:k + 1]), t[k:k + 1]))[0])
+
+
 def test_two_query_blocks_per_wavefront_equal_one():
     """64 rows of the head-dim-48 network run attention with two 32-query blocks per
     wavefront (512 workgroups of 128 queries); four rows at a time take one block per
