@@ -13,7 +13,10 @@
 //     and sum are lane-local plus a single cross-half shuffle;
 //   * the running max is only moved when a block's max exceeds it by more than 2^8 (in
 //     exp2 units), so the rescale of the output accumulators is rare; probabilities
-//     are then at most 256, which bf16 and the fp32 sums carry exactly as well;
+//     are then at most 256, which bf16 and the fp32 sums carry exactly as well. At
+//     head dim 64 (row sums by vector adds) the step's probabilities are formed against
+//     the current max first and the max is only taken when the row sum leaves
+//     [0, 2^64] (softmax_step_sum);
 //   * the probabilities are rounded to bf16 and used directly as the B operand of
 //     O^T = V^T P^T: the MFMA's k-slot order is a permutation of the key order, and V^T
 //     is stored in that permuted key order (vt_pos, written so by the QKV projection),
@@ -291,6 +294,51 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   }
 }
 
+// One step of the online softmax for a 32-query block at head dim 64, where the row sum
+// is kept by vector adds: each lane's 16 scores become probabilities against the running
+// max m2 (exp2 units), added to the lane's row sum lsum and rounded to the bf16 P.V
+// operands pf. The max itself is only taken when the row sum this gives leaves
+// [0, 2^64] on some lane of the block: the first step (no max yet), non-finite scores,
+// or scores above m2 by about 64. Then the block moves to the new max (the output and
+// sum rescaled) and the step's probabilities are recomputed. Up to 2^64 every
+// probability, the sums and the outputs stay far inside fp32 and bf16 range and keep
+// their relative precision, so a max that lags the true one costs nothing, and most
+// steps skip the max reduction and its cross-half exchange.
+template <int DB>
+__device__ __forceinline__ void softmax_step_sum(const f32x16& sc, float sl2, float& m2, float& lsum,
+                                                 f32x16 (&o)[DB], bf16x8 (&pf)[2]) {
+  auto probs = [&]() {
+    float l = lsum;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[ks * 8 + j], sl2, -m2));
+        l += p;
+        pf[ks][j] = (bf16)p;
+      }
+    }
+    return l;
+  };
+  float l = probs();
+  if (__any(!(l <= 0x1p64f))) {
+    float tmax = sc[0];
+#pragma unroll
+    for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[e]);
+    tmax = pair32_max(tmax) * sl2;
+    const float mnew = fmaxf(m2, tmax);
+    const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
+    lsum *= alpha;
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
+    m2 = mnew;
+    l = probs();
+  }
+  lsum = l;
+}
+
 // Head dim 64: the same computation with the K and V^T tiles moved by buffer_load ... lds
 // straight from global memory into a ring of three LDS stages, two steps ahead (no VGPR
 // round trip, no LDS write instructions). Each stage is its own __shared__ variable
@@ -409,30 +457,8 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
       for (int e = 0; e < 16; ++e)
         if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) sc[e] = -INFINITY;
     }
-    float tmax = sc[0];
-#pragma unroll
-    for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[e]);
-    tmax = pair32_max(tmax) * sl2;
-    if (__any(tmax > m2 + kLazy)) {
-      const float mnew = fmaxf(m2, tmax);
-      const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
-      lsum *= alpha;
-#pragma unroll
-      for (int b = 0; b < DB; ++b)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
-      m2 = mnew;
-    }
     bf16x8 pf[2];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sc[ks * 8 + j], sl2, -m2));
-        lsum += p;
-        pf[ks][j] = (bf16)p;
-      }
-    }
+    softmax_step_sum<DB>(sc, sl2, m2, lsum, o, pf);
     // V^T fragment of k-slots 8g..8g+7: keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
     // of this half, which the permuted layout (vt_pos) keeps in one 16-byte chunk,
     // kh*4 + 2 ks + g
@@ -625,31 +651,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
     }
     bf16x8 pf[QB][2];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      float tmax = sc[qb][0];
-#pragma unroll
-      for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[qb][e]);
-      tmax = pair32_max(tmax) * sl2;
-      if (__any(tmax > m2[qb] + kLazy)) {
-        const float mnew = fmaxf(m2[qb], tmax);
-        const float alpha = __builtin_amdgcn_exp2f(m2[qb] - mnew);
-        lsum[qb] *= alpha;
-#pragma unroll
-        for (int b = 0; b < DB; ++b)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[qb][b][e] *= alpha;
-        m2[qb] = mnew;
-      }
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(sc[qb][ks * 8 + j], sl2, -m2[qb]));
-          lsum[qb] += p;
-          pf[qb][ks][j] = (bf16)p;
-        }
-      }
-    }
+    for (int qb = 0; qb < QB; ++qb) softmax_step_sum<DB>(sc[qb], sl2, m2[qb], lsum[qb], o[qb], pf[qb]);
 #pragma unroll
     for (int b = 0; b < DB; ++b) {
       const char* vrow = cur + KCHUNKS * 16 + (b * 32 + l32) * CPR * 16;
