@@ -46,17 +46,17 @@ MI355X_HBM_GBS = 8000.0
 # only for the kernel sources it was measured on (hash below); otherwise traffic is null.
 KERNEL_SOURCES = ("k_gemm.hip", "k_attn.hip", "sf_device.h", "sf_launch.h")
 TRAFFIC = {
-    ("s512", "bf16", "FC2"): {"bytes": 94525009, "sources": "3ba7cf6f59b418bb",
+    ("s512", "bf16", "FC2"): {"bytes": 94524813, "sources": "0b77534450d44176",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512", "bf16", "FC1"): {"bytes": 59991757, "sources": "3ba7cf6f59b418bb",
+    ("s512", "bf16", "FC1"): {"bytes": 59991674, "sources": "0b77534450d44176",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512_large", "bf16", "FC2"): {"bytes": 187429980, "sources": "3ba7cf6f59b418bb",
+    ("s512_large", "bf16", "FC2"): {"bytes": 187881832, "sources": "0b77534450d44176",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_large", "bf16", "FC1"): {"bytes": 133715143, "sources": "3ba7cf6f59b418bb",
+    ("s512_large", "bf16", "FC1"): {"bytes": 133317623, "sources": "0b77534450d44176",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_cfg", "bf16", "FC2"): {"bytes": 383249474, "sources": "3ba7cf6f59b418bb",
+    ("s512_cfg", "bf16", "FC2"): {"bytes": 382178453, "sources": "0b77534450d44176",
                                   "profile": "profiles/stream_step_s512_cfg_bf16.md"},
-    ("s1024", "bf16", "ATTN"): {"bytes": 161856290, "sources": "3ba7cf6f59b418bb",
+    ("s1024", "bf16", "ATTN"): {"bytes": 161879120, "sources": "0b77534450d44176",
                                 "profile": "profiles/stream_step_s1024_bf16.md"},
 }
 
