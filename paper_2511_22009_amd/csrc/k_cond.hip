@@ -22,11 +22,11 @@ constexpr int kGemvSamples = 4;  // samples per pass (inputs held in registers)
 // X, or built as the sinusoids of 1000 t). The RW x 4 row/sample partial sums leave
 // through butterfly reductions of 16 values. One task (RW rows) per wavefront.
 template <typename WT, int NC, int RW, int XMODE>
-__global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
+__device__ __forceinline__ void gemv_body(const GemvArgs& a, int bid) {
   constexpr int E = 16 / sizeof(WT);  // elements per 16-byte chunk
   static_assert(RW * kGemvSamples % 16 == 0, "rows x samples must fill butterfly groups");
   const int lane = threadIdx.x & 63;
-  const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RW;
+  const int j0 = (bid * 4 + (threadIdx.x >> 6)) * RW;
   // the sinusoid mode builds each batch's embedding once per workgroup in LDS (with a
   // barrier), so there every wavefront stays to the end
   if (XMODE == 0 && j0 >= a.R) return;
@@ -124,12 +124,22 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
   }
 }
 
+template <typename WT, int NC, int RW, int XMODE>
+__global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
+  gemv_body<WT, NC, RW, XMODE>(a, blockIdx.x);
+}
+
+// Rows per wavefront: keep the loads of a task within the register file. Eight rows up
+// to three fp32 chunks per lane (a 768-wide fp32 layer: 143 VGPRs, 5.3 against 6.4 us
+// with four rows), four beyond.
+template <typename WT, int NC>
+constexpr int gemv_rows_per_wave() {
+  return NC <= 2 || (NC == 3 && sizeof(WT) == 4) ? 8 : 4;
+}
+
 template <typename WT, int NC>
 static void launch_gemv_nc(const GemvArgs& a, hipStream_t s) {
-  // keep the loads of a task within the register file: eight rows per wavefront up to
-  // three fp32 chunks per lane (a 768-wide fp32 layer: 143 VGPRs, 5.3 against 6.4 us
-  // with four rows), four beyond
-  constexpr int RW = NC <= 2 || (NC == 3 && sizeof(WT) == 4) ? 8 : 4;
+  constexpr int RW = gemv_rows_per_wave<WT, NC>();
   const int tasks = (a.R + RW - 1) / RW;
   if (a.x_mode == 1)
     launch((gemv_kernel<WT, NC, RW, 1>), dim3((tasks + 3) / 4), dim3(256), 0, s, a);
@@ -174,10 +184,10 @@ hipError_t launch_gemv(bool w_bf16, const GemvArgs& a, hipStream_t s) {
 // instead of following each other across the barrier.
 constexpr int kEmbedWgTok = 8;
 
-__global__ __launch_bounds__(256) void embed_p2c4_kernel(EmbedArgs a) {
+__device__ __forceinline__ void embed_p2c4_body(const EmbedArgs& a, int bid) {
   __shared__ float4 px_s[kEmbedWgTok][4];  // token t: feature (2i + j) * 4 + c at [t][f / 4][f % 4]
   const int M = a.rows * a.N;
-  const int m0 = blockIdx.x * kEmbedWgTok;
+  const int m0 = bid * kEmbedWgTok;
   const int tid = threadIdx.x;
   const int gwn = a.W / 2;
   const int d4n = a.D >> 2;
@@ -249,6 +259,8 @@ __global__ __launch_bounds__(256) void embed_p2c4_kernel(EmbedArgs a) {
   }
 }
 
+__global__ __launch_bounds__(256) void embed_p2c4_kernel(EmbedArgs a) { embed_p2c4_body(a, blockIdx.x); }
+
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   const int d4n = a.D >> 2;
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
@@ -280,6 +292,49 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
     launch(embed_p2c4_kernel, dim3((a.rows * a.N + kEmbedWgTok - 1) / kEmbedWgTok), dim3(256), 0, s, a);
   } else {
     launch(embed_kernel, dim3((total + 255) / 256), dim3(256), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+// The adaLN GEMV and the patch embed in one grid. They are independent (the embed does
+// not read the conditioning), and the GEMV's workgroups leave most of the chip idle in
+// their last round (1776 of them at 512^2, three per CU: 2.3 rounds). So the embed's
+// workgroups follow the GEMV's in the same launch, filling that round, instead of
+// running as a launch of their own. Each part computes exactly what its own kernel does.
+template <typename WT, int NC, int RW>
+__global__ __launch_bounds__(256) void gemv_embed_kernel(GemvArgs g, EmbedArgs e, int n_gemv) {
+  if ((int)blockIdx.x < n_gemv)
+    gemv_body<WT, NC, RW, 0>(g, blockIdx.x);
+  else
+    embed_p2c4_body(e, blockIdx.x - n_gemv);
+}
+
+bool gemv_embed_supported(bool w_bf16, const GemvArgs& g, const EmbedArgs& e) {
+  const int E = w_bf16 ? 8 : 4;
+  const int nc = (g.K / E + 63) / 64;
+  return g.x_mode == 0 && e.p == 2 && e.C == 4 && g.K % E == 0 && nc >= 1 && nc <= 3 &&
+         (size_t)g.R * g.K * (w_bf16 ? 2 : 4) < (1ull << 31);
+}
+
+template <typename WT, int NC>
+static void launch_gemv_embed_nc(const GemvArgs& g, const EmbedArgs& e, hipStream_t s) {
+  constexpr int RW = gemv_rows_per_wave<WT, NC>();
+  const int n_gemv = ((g.R + RW - 1) / RW + 3) / 4;
+  const int n_embed = (e.rows * e.N + kEmbedWgTok - 1) / kEmbedWgTok;
+  launch((gemv_embed_kernel<WT, NC, RW>), dim3(n_gemv + n_embed), dim3(256), 0, s, g, e, n_gemv);
+}
+
+hipError_t launch_gemv_embed(bool w_bf16, const GemvArgs& g, const EmbedArgs& e, hipStream_t s) {
+  if (!gemv_embed_supported(w_bf16, g, e)) return hipErrorInvalidValue;
+  const int nc = (g.K / (w_bf16 ? 8 : 4) + 63) / 64;
+  if (w_bf16) {
+    if (nc == 1) launch_gemv_embed_nc<bf16, 1>(g, e, s);
+    else if (nc == 2) launch_gemv_embed_nc<bf16, 2>(g, e, s);
+    else launch_gemv_embed_nc<bf16, 3>(g, e, s);
+  } else {
+    if (nc == 1) launch_gemv_embed_nc<float, 1>(g, e, s);
+    else if (nc == 2) launch_gemv_embed_nc<float, 2>(g, e, s);
+    else launch_gemv_embed_nc<float, 3>(g, e, s);
   }
   return hipGetLastError();
 }

@@ -75,6 +75,11 @@ struct EmbedArgs {
   int rows, C, H, W, p, D, N;
 };
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+// The last adaLN projection (x_mode 0) and the patch embed in one launch, each part with
+// the arithmetic of its own kernel. Supported for 2x2 patches of 4 channels and GEMV
+// rows of at most three chunks per lane; otherwise hipErrorInvalidValue, nothing launched.
+bool gemv_embed_supported(bool w_bf16, const GemvArgs& g, const EmbedArgs& e);
+hipError_t launch_gemv_embed(bool w_bf16, const GemvArgs& g, const EmbedArgs& e, hipStream_t s);
 
 // ---- context entries of the cross-attention K/V ------------------------------------
 // The keys and values of a context depend on the context and the weights only, so they

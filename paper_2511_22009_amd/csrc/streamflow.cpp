@@ -375,8 +375,11 @@ int timed(sf_model* m, int kc, hipStream_t s, F&& launch) {
   } while (0)
 
 // Per-sample conditioning: t[k] -> adaLN table row k (width modw). hid and svec hold the
-// timestep MLP's hidden layer and SiLU(c) ([n][D] each).
-int run_modulation(sf_model* m, const float* t, int n, float* table, hipStream_t s, float* hid, float* svec) {
+// timestep MLP's hidden layer and SiLU(c) ([n][D] each). With `embed`, the patch embed
+// runs in the same launch as the adaLN projections where that kernel supports it, and
+// *embedded says whether it did.
+int run_modulation(sf_model* m, const float* t, int n, float* table, hipStream_t s, float* hid, float* svec,
+                   const sf::EmbedArgs* embed = nullptr, bool* embedded = nullptr) {
   const Header& h = m->hd;
   return timed(m, SF_KC_TEMB, s, [&]() -> hipError_t {
     sf::GemvArgs g{};
@@ -416,8 +419,18 @@ int run_modulation(sf_model* m, const float* t, int n, float* table, hipStream_t
     g3.R = m->modw;
     g3.Y = table;
     g3.ldy = m->modw;
+    if (embed && sf::gemv_embed_supported(m->bf16, g3, *embed)) {
+      *embedded = true;
+      return sf::launch_gemv_embed(m->bf16, g3, *embed, s);
+    }
     return sf::launch_gemv(m->bf16, g3, s);
   });
+}
+
+bool any_timing(const sf_model* m) {
+  for (const Timing& tm : m->timing)
+    if (tm.on) return true;
+  return false;
 }
 
 sf::GemmArgs gemm_base(const void* A, int lda, const void* B, int ldb, int M, int N, int K, const float* bias) {
@@ -440,11 +453,12 @@ int run_network(sf_model* m, const float* x, const float* t, int n_lat, int rows
                 int nblocks, float* head_out, hipStream_t s, bool table_ready = false) {
   const Header& h = m->hd;
   const int D = h.D, N = m->N, M = rows * N;
-  if (!table_ready) SF_TRY(run_modulation(m, t, n_lat, m->table, s, m->hid, m->svec));
-  SF_TRY(timed(m, SF_KC_EMBED, s, [&]() {
-    sf::EmbedArgs e{x, n_lat, m->W_pe, m->b_pe, m->pos, m->h, rows, (int)h.C, (int)h.H, (int)h.W, (int)h.p, D, N};
-    return sf::launch_embed(e, s);
-  }));
+  const sf::EmbedArgs emb{x, n_lat, m->W_pe, m->b_pe, m->pos, m->h, rows, (int)h.C, (int)h.H, (int)h.W, (int)h.p, D, N};
+  // the embed shares the adaLN projections' launch unless per-class times are taken
+  bool embedded = false;
+  if (!table_ready)
+    SF_TRY(run_modulation(m, t, n_lat, m->table, s, m->hid, m->svec, any_timing(m) ? nullptr : &emb, &embedded));
+  if (!embedded) SF_TRY(timed(m, SF_KC_EMBED, s, [&]() { return sf::launch_embed(emb, s); }));
   const sf::FastDiv div_n = sf::make_fastdiv(N), div_d = sf::make_fastdiv(D), div_dh = sf::make_fastdiv(m->dh);
   const sf::FastDiv div_ctx = sf::make_fastdiv(h.has_cross ? m->ctx_lp : 1);
   const int* kv_map = nullptr;
@@ -631,12 +645,6 @@ std::vector<char> call_key(const sf_model* m, int kind, const void* a, const voi
     key_put(k, cond->guidance);
   }
   return k;
-}
-
-bool any_timing(const sf_model* m) {
-  for (const Timing& tm : m->timing)
-    if (tm.on) return true;
-  return false;
 }
 
 void drop_graphs(sf_model* m) {

@@ -398,6 +398,28 @@ def test_two_query_blocks_per_wavefront_equal_one():
         np.testing.assert_array_equal(full[k0:k0 + 4], host(m.velocity(dev(x[k0:k0 + 4]), t[k0:k0 + 4])))
 
 
+@pytest.mark.parametrize("name,prec", [("tiny", "fp32"), ("tiny", "bf16"), ("dh72", "fp32"),
+                                       ("dh64", "bf16"), ("tiny_cfg", "bf16")])
+def test_embed_in_modulation_launch_equals_own_launch(name, prec):
+    """The patch embed shares the launch of the last adaLN projection unless per-class
+    kernel times are taken; with the embed's timing on it runs as a launch of its own.
+    Same bits either way, also with guidance (twice as many embedded rows as table rows)."""
+    from paper_2511_22009_amd import Cond, KernelClass, Model, Precision
+    from conftest import blob_for
+    cfg = W.get_config(name)
+    B = cfg.K
+    x, t = W.latents(cfg, B, seed=81), np.random.default_rng(82).uniform(0.0, 1.0, B).astype(np.float32)
+    m = Model(blob_for(name, None), Precision[prec.upper()], 2 * B)
+    cond = Cond(dev(W.context(cfg, B)), dev(W.null_context(cfg)), cfg.guidance) if cfg.has_cross else None
+    shared = host(m.velocity(dev(x), t, cond))
+    m.timing_enable(KernelClass.EMBED, True)
+    own = host(m.velocity(dev(x), t, cond))
+    m.timing_enable(KernelClass.EMBED, False)
+    np.testing.assert_array_equal(shared, own)
+    np.testing.assert_array_equal(shared, host(m.velocity(dev(x), t, cond)))
+    m.close()
+
+
 @pytest.mark.parametrize("prec", PRECS)
 def test_max_rows_guided_velocity_parity(prec):
     """32 text-conditioned samples with guidance fill all 64 rows (cond and uncond)."""
