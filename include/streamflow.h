@@ -183,6 +183,14 @@ enum { SF_BUF_H = 0, SF_BUF_ACT, SF_BUF_Q, SF_BUF_K, SF_BUF_VT, SF_BUF_ATTN, SF_
  * `dst` (enqueued on hip_stream). SF_E_INVAL if bytes exceeds the buffer. */
 int sf_debug_read(sf_model* m, int buffer, void* dst, size_t bytes, void* hip_stream);
 
+/* Test hook: the model's self-attention (Sec. 3.2's network, one layer's
+ * softmax(q k^T / sqrt(dh)) v per row and head) on caller buffers, in the layouts and
+ * element type of the internal buffers above: q, k device [rows][heads][N][dh], vT device
+ * [rows][heads][dh][vt_ld] (keys permuted when vt_key_perm is 1, columns past N zero),
+ * o device [rows][N][D] output. rows 1..SF_MAX_ROWS (independent of max_rows). The
+ * same kernels as the network call for that many rows. */
+int sf_attention(sf_model* m, const void* q, const void* k, const void* vT, void* o, int rows, void* hip_stream);
+
 /* Kernel classes for event timing. */
 enum {
   SF_KC_TEMB = 0,   /* timestep embedding, MLP and adaLN projections */

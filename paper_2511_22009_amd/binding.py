@@ -85,6 +85,7 @@ _SIGS = {
     "sf_modulation_noalloc": (_I, [_P, _P, _I, _P, _P]),
     "sf_residual": (_I, [_P, _P, _P, _I, _P, _I, _P, _P]),
     "sf_debug_read": (_I, [_P, _I, _P, ctypes.c_size_t, _P]),
+    "sf_attention": (_I, [_P, _P, _P, _P, _P, _I, _P]),
     "sf_timing_enable": (_I, [_P, _I, _I]),
     "sf_timing_read": (_I, [_P, _I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_long)]),
     "sf_graph_enable": (_I, [_P, _I]),
@@ -277,6 +278,26 @@ class Model:
                                             out.numel() * out.element_size(), self._stream(stream)),
                "sf_debug_read")
         return out.float()
+
+    def attention(self, q, k, vT, stream=None):
+        """The model's self-attention on caller tensors (see sf_attention): q, k
+        [rows, heads, N, dh], vT [rows, heads, dh, vt_ld] in the compute type (bf16 in
+        bf16 mode, else float32), contiguous, on the GPU. Returns o [rows, N, D]."""
+        import torch
+        inf = self.info
+        rows = q.shape[0]
+        dt = torch.float32 if inf["precision"] == int(Precision.FP32) else torch.bfloat16
+        dh = inf["D"] // inf["heads"]
+        want = {"q": (q, (rows, inf["heads"], inf["tokens"], dh)), "k": (k, (rows, inf["heads"], inf["tokens"], dh)),
+                "vT": (vT, (rows, inf["heads"], dh, inf["vt_ld"]))}
+        for name, (ten, shape) in want.items():
+            if tuple(ten.shape) != shape or ten.dtype != dt or not ten.is_cuda or not ten.is_contiguous():
+                raise ValueError(f"{name}: expected contiguous {dt} {shape} on the GPU")
+        o = torch.empty((rows, inf["tokens"], inf["D"]), dtype=dt, device=q.device)
+        _check(load_library().sf_attention(self._h, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
+                                           ctypes.c_void_p(vT.data_ptr()), ctypes.c_void_p(o.data_ptr()), rows,
+                                           self._stream(stream)), "sf_attention")
+        return o
 
     def set_scheduler(self, windows=4, train_steps=1000, beta_start=0.00085, beta_end=0.012, eps=1e-6):
         """Read the network output as a noise prediction and update with PeRFlow's time

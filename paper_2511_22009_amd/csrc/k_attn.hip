@@ -14,9 +14,9 @@
 //   * the running max is only moved when a block's max exceeds it by more than 2^8 (in
 //     exp2 units), so the rescale of the output accumulators is rare; probabilities
 //     are then at most 256, which bf16 and the fp32 sums carry exactly as well. At
-//     head dim 64 (row sums by vector adds) the step's probabilities are formed against
-//     the current max first and the max is only taken when the row sum leaves
-//     [0, 2^64] (softmax_step_sum);
+//     head dim 64 (row sums by vector adds) q is scaled into exp2 units once, the
+//     probabilities are formed against an offset that starts at 0, and a max is only
+//     taken when a row sum leaves [2^-64, 2^64] (softmax_step_sum);
 //   * the probabilities are rounded to bf16 and used directly as the B operand of
 //     O^T = V^T P^T: the MFMA's k-slot order is a permutation of the key order, and V^T
 //     is stored in that permuted key order (vt_pos, written so by the QKV projection),
@@ -295,48 +295,61 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 }
 
 // One step of the online softmax for a 32-query block at head dim 64, where the row sum
-// is kept by vector adds: each lane's 16 scores become probabilities against the running
-// max m2 (exp2 units), added to the lane's row sum lsum and rounded to the bf16 P.V
-// operands pf. The max itself is only taken when the row sum this gives leaves
-// [0, 2^64] on some lane of the block: the first step (no max yet), non-finite scores,
-// or scores above m2 by about 64. Then the block moves to the new max (the output and
-// sum rescaled) and the step's probabilities are recomputed. Up to 2^64 every
-// probability, the sums and the outputs stay far inside fp32 and bf16 range and keep
-// their relative precision, so a max that lags the true one costs nothing, and most
-// steps skip the max reduction and its cross-half exchange.
+// is kept by vector adds. The scores arrive in exp2 units (q was multiplied by
+// scale * log2 e), and each lane's 16 of them become probabilities against the query's
+// offset m2: p = 2^(s - m2), added to the lane's row sum lsum and rounded to the bf16
+// P.V operands pf. The offset starts at 0 and is left alone while every row sum of the
+// block stays in [2^-64, 2^64]; while it is 0 for all queries of the wavefront the
+// subtraction is skipped (s - 0 is s: the same bits). A softmax does not depend on the
+// offset, and inside that range every probability, sum and output keeps its full
+// relative precision, so no max is taken at all in the usual case. When a sum leaves the
+// range (scores above about 64 or all below about -64 so far, non-finite scores), the
+// step takes the max over both lane halves and moves the offset: to the max, for a query
+// with no probability mass yet (which may lower it), else up to the max if that is
+// larger, with the accumulated output and sum rescaled; then the probabilities are
+// formed again. The offset is the same on both lane halves of a query at all times.
 template <int DB>
-__device__ __forceinline__ void softmax_step_sum(const f32x16& sc, float sl2, float& m2, float& lsum,
-                                                 f32x16 (&o)[DB], bf16x8 (&pf)[2]) {
-  auto probs = [&]() {
+__device__ __forceinline__ void softmax_step_sum(const f32x16& sc, float& m2, float& lsum, f32x16 (&o)[DB],
+                                                 bf16x8 (&pf)[2]) {
+  auto probs = [&](auto shifted) {
     float l = lsum;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sc[ks * 8 + j], sl2, -m2));
+        const float x = sc[ks * 8 + j];
+        const float p = __builtin_amdgcn_exp2f(decltype(shifted)::value ? x - m2 : x);
         l += p;
         pf[ks][j] = (bf16)p;
       }
     }
     return l;
   };
-  float l = probs();
-  if (__any(!(l <= 0x1p64f))) {
+  float l = __all(m2 == 0.0f) ? probs(std::false_type{}) : probs(std::true_type{});
+  if (__any(!(l <= 0x1p64f && l >= 0x1p-64f))) {
     float tmax = sc[0];
 #pragma unroll
     for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[e]);
-    tmax = pair32_max(tmax) * sl2;
-    const float mnew = fmaxf(m2, tmax);
-    const float alpha = __builtin_amdgcn_exp2f(m2 - mnew);
+    tmax = pair32_max(tmax);
+    const bool empty = pair32_sum(lsum) == 0.0f;  // nothing accumulated for this query yet
+    const float mnew = empty ? tmax : fmaxf(m2, tmax);
+    const float alpha = empty ? 0.0f : __builtin_amdgcn_exp2f(m2 - mnew);
     lsum *= alpha;
 #pragma unroll
     for (int b = 0; b < DB; ++b)
 #pragma unroll
       for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
     m2 = mnew;
-    l = probs();
+    l = probs(std::true_type{});
   }
   lsum = l;
+}
+
+// q fragments of head dim 64 scaled into exp2 units: bf16(q * scale * log2 e), once per
+// wavefront, so the score MFMA returns the exponents the softmax takes.
+__device__ __forceinline__ void scale_q(bf16x8& q, float sl2) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) q[e] = (bf16)((float)q[e] * sl2);
 }
 
 // Head dim 64: the same computation with the K and V^T tiles moved by buffer_load ... lds
@@ -387,12 +400,14 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   const bf16* Vt = (const bf16*)a.vT + kr * a.v_rs + (size_t)head * DH * a.ldv;
   const int qi = qblk * kQB + qg * 32 + l32;
 
+  const float sl2 = a.scale * 1.4426950408889634f;
   bf16x8 qf[DHC];
   const __amdgpu_buffer_rsrc_t q_src = buffer_rsrc(Q, (uint32_t)a.Nq * DH * 2);
 #pragma unroll
   for (int kk = 0; kk < DHC; ++kk) {
     const u32x4 w = buffer_load16(q_src, qi < a.Nq ? (qi * DH + kk * 16 + g * 8) * 2 : kOffOOB);
     qf[kk] = __builtin_bit_cast(bf16x8, w);
+    scale_q(qf[kk], sl2);
   }
 
   // load i of a thread fills chunk position p = i * 256 + tid of a stage: K row (key)
@@ -425,8 +440,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   for (int b = 0; b < DB; ++b)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[b][e] = 0.0f;
-  float m2 = -INFINITY, lsum = 0.0f;
-  const float sl2 = a.scale * 1.4426950408889634f;
+  float m2 = 0.0f, lsum = 0.0f;
   const int sw = dma_swz<CPR>(l32);  // the swizzle of every row this lane reads
   const int krow = (kh * kKH + l32) * CPR;
 
@@ -458,7 +472,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
         if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) sc[e] = -INFINITY;
     }
     bf16x8 pf[2];
-    softmax_step_sum<DB>(sc, sl2, m2, lsum, o, pf);
+    softmax_step_sum<DB>(sc, m2, lsum, o, pf);
     // V^T fragment of k-slots 8g..8g+7: keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
     // of this half, which the permuted layout (vt_pos) keeps in one 16-byte chunk,
     // kh*4 + 2 ks + g
@@ -501,14 +515,14 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   }
   __syncthreads();
   if (kh == 1) return;
+  // key half 0 always holds key 0; half 1 saw no key when there are at most 32 (its
+  // zeros are then left out by selects, and its offset is not used)
+  const bool other = kKH < a.Nk;
   const float m2b = mg[DB * 16 * 64 + lane];
-  const float mnew = fmaxf(m2, m2b);
-  const float a0 = m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2 - mnew);
-  const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
-  // a half that saw no key (max still -inf) holds zeros and is left out by selects,
-  // not multiplied by a zero weight
-  const bool own = m2 != -INFINITY, other = m2b != -INFINITY;
-  lsum = (own ? lsum * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
+  const float mnew = other ? fmaxf(m2, m2b) : m2;
+  const float a0 = __builtin_amdgcn_exp2f(m2 - mnew);
+  const float a1 = other ? __builtin_amdgcn_exp2f(m2b - mnew) : 0.0f;
+  lsum = lsum * a0 + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
   lsum = pair32_sum(lsum);
   const float inv = 1.0f / lsum;
   if (qi < a.Nq) {
@@ -522,7 +536,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int e = e4 * 4 + q;
-          w[q] = ((own ? o[b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
+          w[q] = (o[b][e] * a0 + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
         }
         *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
       }
@@ -574,6 +588,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) qi[qb] = qblk * kQB2 + qg * 64 + qb * 32 + l32;
 
+  const float sl2 = a.scale * 1.4426950408889634f;
   bf16x8 qf[QB][DHC];
   const __amdgpu_buffer_rsrc_t q_src = buffer_rsrc(Q, (uint32_t)a.Nq * DH * 2);
 #pragma unroll
@@ -582,6 +597,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
     for (int kk = 0; kk < DHC; ++kk) {
       const u32x4 w = buffer_load16(q_src, qi[qb] < a.Nq ? (qi[qb] * DH + kk * 16 + g * 8) * 2 : kOffOOB);
       qf[qb][kk] = __builtin_bit_cast(bf16x8, w);
+      scale_q(qf[qb][kk], sl2);
     }
 
   int goff[LPT];
@@ -612,10 +628,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
   float m2[QB], lsum[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    m2[qb] = -INFINITY;
+    m2[qb] = 0.0f;
     lsum[qb] = 0.0f;
   }
-  const float sl2 = a.scale * 1.4426950408889634f;
   const int sw = dma_swz<CPR>(l32);
   const int krow = (kh * kKH + l32) * CPR;
 
@@ -651,7 +666,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
     }
     bf16x8 pf[QB][2];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) softmax_step_sum<DB>(sc[qb], sl2, m2[qb], lsum[qb], o[qb], pf[qb]);
+    for (int qb = 0; qb < QB; ++qb) softmax_step_sum<DB>(sc[qb], m2[qb], lsum[qb], o[qb], pf[qb]);
 #pragma unroll
     for (int b = 0; b < DB; ++b) {
       const char* vrow = cur + KCHUNKS * 16 + (b * 32 + l32) * CPR * 16;
@@ -695,12 +710,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
     }
     __syncthreads();
     if (kh == 0) {
+      // as in attn_bf16_dma64_kernel: half 1 saw keys only when there are more than 32
+      const bool other = kKH < a.Nk;
       const float m2b = mg[DB * 16 * 64 + lane];
-      const float mnew = fmaxf(m2[qb], m2b);
-      const float a0 = m2[qb] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2[qb] - mnew);
-      const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
-      const bool own = m2[qb] != -INFINITY, other = m2b != -INFINITY;
-      float ls = (own ? lsum[qb] * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
+      const float mnew = other ? fmaxf(m2[qb], m2b) : m2[qb];
+      const float a0 = __builtin_amdgcn_exp2f(m2[qb] - mnew);
+      const float a1 = other ? __builtin_amdgcn_exp2f(m2b - mnew) : 0.0f;
+      float ls = lsum[qb] * a0 + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
       ls = pair32_sum(ls);
       const float inv = 1.0f / ls;
       if (qi[qb] < a.Nq) {
@@ -714,7 +730,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const int e = e4 * 4 + q;
-              w[q] = ((own ? o[qb][b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
+              w[q] = (o[qb][b][e] * a0 + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
             }
             *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
           }

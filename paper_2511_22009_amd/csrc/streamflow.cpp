@@ -920,6 +920,15 @@ int sf_residual(sf_model* m, const float* x, const float* t, int B, const sf_con
   return SF_OK;
 }
 
+int sf_attention(sf_model* m, const void* q, const void* k, const void* vT, void* o, int rows, void* stream) {
+  if (!m) return SF_E_NOTLOADED;
+  if (!q || !k || !vT || !o || rows < 1 || rows > SF_MAX_ROWS) return SF_E_INVAL;
+  const Header& h = m->hd;
+  sf::AttnArgs a{q, k, vT, o, rows, (int)h.heads, m->N, m->N, m->dh, m->ldv, (int)h.D,
+                 (float)(1.0 / std::sqrt((double)m->dh)), m->vperm};
+  return sf::launch_attention(m->bf16, a, (hipStream_t)stream) == hipSuccess ? SF_OK : SF_E_HIP;
+}
+
 int sf_debug_read(sf_model* m, int buffer, void* dst, size_t bytes, void* stream) {
   if (!m) return SF_E_NOTLOADED;
   if (!dst) return SF_E_INVAL;

@@ -81,6 +81,7 @@ def test_calls_reject_null_handle_and_arguments():
     assert L.sf_euler_shift(None, dummy, dummy, t, 4, dummy, None, None) == -3
     assert L.sf_modulation(None, t, 4, dummy, None) == -3
     assert L.sf_residual(None, dummy, t, 4, None, 0, dummy, None) == -3
+    assert L.sf_attention(None, dummy, dummy, dummy, dummy, 1, None) == -3
     assert L.sf_timing_enable(None, 0, 1) == -3
     assert L.sf_get_info(None, None) == -3
     L.sf_free(None)

@@ -72,3 +72,41 @@ def test_block0_intermediates(name, prec):
     assert worst["fc1_iso"] <= ISO[prec], worst
     for key in ("q", "k", "v", "attn", "ln2", "mlp", "h_out"):
         assert worst[key] <= TOL[prec], worst
+
+
+@pytest.mark.parametrize("D,heads", [(128, 2), (144, 2), (96, 2), (64, 2)], ids=["dh64", "dh72", "dh48", "dh32"])
+def test_attention_scores_far_from_zero(D, heads):
+    """Scores whose level per query lies far outside [-64, 64] in exp2 units, on both
+    sides: every key entry is 128 plus a small exact integer step, so a query's scores are
+    a large offset (its product with the shared part, spread about +-185 exp2 units over
+    the queries) plus a spread of a few units between keys. Softmax does not depend on the
+    offset, so the result is well conditioned, while the kernels' online softmax meets
+    sums that overflow and underflow and maxima far from zero. bf16 attention alone
+    (sf_attention) on exact bf16 inputs against the oracle's fp64 softmax: 64 rows run the
+    two-query-block kernels, four rows the one-block ones, and the four rows both ran
+    agree bit for bit."""
+    from paper_2511_22009_amd import Model, Precision
+    cfg = W.Config(f"attn{D}", C=4, H=32, W=64, p=2, D=D, L=1, heads=heads, mlp=128)
+    m = Model(W.make_blob(cfg), Precision.BF16, 64)
+    N, dh, ldv, R = cfg.N, D // heads, m.info["vt_ld"], 64
+    rng = np.random.default_rng(91)
+    q = rng.standard_normal((R, heads, N, dh))
+    k = 128.0 + rng.integers(-4, 5, (R, heads, N, dh))
+    v = rng.standard_normal((R, heads, N, dh))
+    qb, kb, vb = (torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16) for a in (q, k, v))
+    q64, k64, v64 = (a.float().numpy().astype(np.float64) for a in (qb, kb, vb))
+    # the inputs are what this test says: offsets beyond +-64 exp2 units for most queries
+    off = np.einsum("rhnd,d->rhn", q64, np.full(dh, 128.0)) / np.sqrt(dh) / np.log(2.0)
+    assert (off > 64).mean() > 0.3 and (off < -64).mean() > 0.3
+    tok = np.arange(N)
+    col = (tok & ~12) | ((tok & 4) << 1) | ((tok & 8) >> 1) if m.info["vt_key_perm"] else tok
+    vT = torch.zeros((R, heads, dh, ldv), dtype=torch.bfloat16)
+    vT[..., torch.from_numpy(col)] = vb.transpose(2, 3)
+    full = m.attention(qb.cuda(), kb.cuda(), vT.cuda()).float()
+    part = m.attention(qb[:4].contiguous().cuda(), kb[:4].contiguous().cuda(), vT[:4].contiguous().cuda()).float()
+    full, part = host(full), host(part)
+    flat = lambda a: a.transpose(1, 0, 2).reshape(N, D)  # noqa: E731  [heads, N, dh] -> [N, D]
+    errs = [rel_l2(full[r], oracle.attention(flat(q64[r]), flat(k64[r]), flat(v64[r]), heads)) for r in range(R)]
+    assert max(errs) <= ISO["bf16"], max(errs)
+    np.testing.assert_array_equal(full[:4], part)
+    m.close()
