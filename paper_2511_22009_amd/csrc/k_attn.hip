@@ -11,12 +11,12 @@
 //   * scores are computed transposed, S^T = K Q^T, so the MFMA result gives each lane
 //     ONE query (column l%32) and 16 of the 32 keys of the block: the running max
 //     and sum are lane-local plus a single cross-half shuffle;
-//   * the running max is only moved when a block's max exceeds it by more than 2^8 (in
-//     exp2 units), so the rescale of the output accumulators is rare; probabilities
-//     are then at most 256, which bf16 and the fp32 sums carry exactly as well. At
-//     head dim 64 (row sums by vector adds) q is scaled into exp2 units once, the
-//     probabilities are formed against an offset that starts at 0, and a max is only
-//     taken when a row sum leaves [2^-64, 2^64] (softmax_step_sum);
+//   * q is scaled into exp2 units (times scale * log2 e, rounded to bf16) once per
+//     wavefront, and the probabilities 2^(s - m2) are formed against a per-query offset
+//     m2 that starts at 0: while it is 0 for the whole wavefront, a probability is one
+//     exp2 of the score. The offset only moves when the scores would leave the range
+//     where probabilities, sums and outputs keep their precision (softmax_step_lazy,
+//     and at head dim 64, where the row sum is kept by vector adds, softmax_step_sum);
 //   * the probabilities are rounded to bf16 and used directly as the B operand of
 //     O^T = V^T P^T: the MFMA's k-slot order is a permutation of the key order, and V^T
 //     is stored in that permuted key order (vt_pos, written so by the QKV projection),
@@ -31,7 +31,82 @@ namespace sf {
 
 constexpr int kKH = 32;    // keys per half per step
 constexpr int kQB = 64;    // queries per workgroup
-constexpr float kLazy = 8.0f;  // max drift (exp2 units) tolerated before a rescale
+constexpr float kOffSlack = 64.0f;  // scores (exp2 units) may pass the offset by this much
+
+// q fragments scaled into exp2 units: bf16(q * scale * log2 e), once per wavefront, so
+// the score MFMA returns the exponents the softmax takes.
+__device__ __forceinline__ void scale_q(bf16x8& q, float sl2) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) q[e] = (bf16)((float)q[e] * sl2);
+}
+
+// The probabilities of one 32-query block's step: 2^(s - m2) for the lane's 16 scores
+// (SHIFT false: 2^s, for a block whose offset is 0; s - 0 is s, so both give the same
+// bits), added to l (SUM) and rounded to the bf16 P.V operands pf.
+template <bool SHIFT, bool SUM>
+__device__ __forceinline__ void block_probs(const f32x16& s, float m2, float& l, bf16x8 (&pf)[2]) {
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float x = s[ks * 8 + j];
+      const float p = __builtin_amdgcn_exp2f(SHIFT ? x - m2 : x);
+      if constexpr (SUM) l += p;
+      pf[ks][j] = (bf16)p;
+    }
+  }
+}
+
+// The probabilities of the QB query blocks of a wavefront, without the subtraction when
+// every offset of the wavefront is 0 (one uniform branch for all blocks, so the blocks'
+// chains stay interleaved).
+template <bool SUM, int QB>
+__device__ __forceinline__ void wave_probs(const f32x16 (&s)[QB], const float (&m2)[QB], float (&l)[QB],
+                                           bf16x8 (&pf)[QB][2]) {
+  bool zero = true;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) zero = zero && m2[qb] == 0.0f;
+  if (__all(zero)) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) block_probs<false, SUM>(s[qb], m2[qb], l[qb], pf[qb]);
+  } else {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) block_probs<true, SUM>(s[qb], m2[qb], l[qb], pf[qb]);
+  }
+}
+
+// One step of the online softmax for QB 32-query blocks (scores s in exp2 units; a
+// lane holds one query and 16 keys of each block). Each block's step max (over both
+// lane halves) decides whether its offset m2 moves: up to the max when that passes the
+// offset by more than kOffSlack, and, at the wavefront's first step (first: nothing
+// accumulated yet), also down to it when it lies more than kOffSlack below. The
+// accumulated output (and row sum, SUM) are rescaled when it moves. Then the
+// probabilities 2^(s - m2) are formed, added to lsum (SUM; otherwise the ones row of
+// V^T sums them in the MFMA) and rounded for P.V. Probabilities stay at most 2^64 and a
+// query's largest one at least 2^-64, so everything keeps its relative precision in fp32
+// and bf16; the offset is the same on both lane halves of a query at all times.
+template <bool SUM, int QB, int DB>
+__device__ __forceinline__ void softmax_step_lazy(const f32x16 (&s)[QB], bool first, float (&m2)[QB],
+                                                  float (&lsum)[QB], f32x16 (&o)[QB][DB], bf16x8 (&pf)[QB][2]) {
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    float tmax = s[qb][0];
+#pragma unroll
+    for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, s[qb][e]);
+    tmax = pair32_max(tmax);
+    if (__any(tmax > m2[qb] + kOffSlack || (first && tmax < m2[qb] - kOffSlack))) {
+      const float mnew = first ? tmax : fmaxf(m2[qb], tmax);
+      const float alpha = first ? 0.0f : __builtin_amdgcn_exp2f(m2[qb] - mnew);
+      if constexpr (SUM) lsum[qb] *= alpha;
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[qb][b][e] *= alpha;
+      m2[qb] = mnew;
+    }
+  }
+  wave_probs<SUM>(s, m2, lsum, pf);
+}
 
 // DHC = ceil(dh/16) contraction chunks, DB = ceil(dh/32) dh blocks. SUMROW (dh not a
 // multiple of 32, so the last dh block has zero rows): row DB*32 - 8 of every V^T tile
@@ -85,6 +160,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   // never written by the staging
   for (int i = tid; i < TILE_BYTES / 16; i += 256) ((u32x4*)smem)[i] = u32x4{0u, 0u, 0u, 0u};
 
+  const float sl2 = a.scale * 1.4426950408889634f;  // scores -> exp2 units
   bf16x8 qf[QB][DHC];
   const __amdgpu_buffer_rsrc_t q_src = buffer_rsrc(Q, (uint32_t)a.Nq * dh * 2);
 #pragma unroll
@@ -94,6 +170,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       const int d0 = kk * 16 + g * 8;
       const u32x4 w = buffer_load16(q_src, (qi[qb] < a.Nq && d0 < dh) ? (qi[qb] * dh + d0) * 2 : kOffOOB);
       qf[qb][kk] = __builtin_bit_cast(bf16x8, w);
+      scale_q(qf[qb][kk], sl2);
     }
 
   // staging map, fixed per thread: K chunk c = (key 0..63, 16-byte column); V^T chunk
@@ -146,13 +223,12 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     for (int b = 0; b < DB; ++b)
 #pragma unroll
       for (int e = 0; e < 16; ++e) o[qb][b][e] = 0.0f;
-  float m2[QB], lsum[QB];                          // running max in exp2 units, partial sum
+  float m2[QB], lsum[QB];                          // offset in exp2 units, partial sum
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    m2[qb] = -INFINITY;
+    m2[qb] = 0.0f;
     lsum[qb] = 0.0f;
   }
-  const float sl2 = a.scale * 1.4426950408889634f;  // scores -> exp2 units
 
   const int nsteps = (a.Nk + 2 * kKH - 1) / (2 * kKH);
   constexpr int kSumRow = DB * 32 - 8;
@@ -190,7 +266,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][kk], s[qb], 0, 0, 0);
       }
-      // s[qb][e]: query l32 of block qb, key kv0 + (e/4)*8 + g*4 + e%4, raw (unscaled).
+      // s[qb][e]: query l32 of block qb, key kv0 + (e/4)*8 + g*4 + e%4, in exp2 units.
       // Only the last, ragged step needs the key mask.
       if (kv0 + kKH > a.Nk) {
 #pragma unroll
@@ -200,32 +276,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
             if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) s[qb][e] = -INFINITY;
       }
       bf16x8 pf[QB][2];
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        float tmax = s[qb][0];
-#pragma unroll
-        for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, s[qb][e]);
-        tmax = pair32_max(tmax) * sl2;
-        if (__any(tmax > m2[qb] + kLazy)) {
-          const float mnew = fmaxf(m2[qb], tmax);
-          const float alpha = __builtin_amdgcn_exp2f(m2[qb] - mnew);
-          lsum[qb] *= alpha;
-#pragma unroll
-          for (int b = 0; b < DB; ++b)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) o[qb][b][e] *= alpha;
-          m2[qb] = mnew;
-        }
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(s[qb][ks * 8 + j], sl2, -m2[qb]));
-            if constexpr (!SUMROW) lsum[qb] += p;
-            pf[qb][ks][j] = (bf16)p;
-          }
-        }
-      }
+      softmax_step_lazy<!SUMROW>(s, it == 0, m2, lsum, o, pf);
       // V^T fragment of k-slots 8g..8g+7 (keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
       // of this half): one 16-byte read in the permuted key layout (vt_pos)
 #pragma unroll
@@ -265,14 +316,14 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     }
     __syncthreads();
     if (kh == 1) continue;
+    // key half 0 always holds key 0; half 1 saw no key when there are at most 32 (its
+    // zeros are then left out by selects, and its offset is not used)
+    const bool other = kKH < a.Nk;
     const float m2b = mg[DB * 16 * 64 + lane];
-    const float mnew = fmaxf(m2[qb], m2b);
-    const float a0 = m2[qb] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2[qb] - mnew);
-    const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
-    // a half that saw no key (max still -inf) holds zeros and is left out by selects,
-    // not multiplied by a zero weight
-    const bool own = m2[qb] != -INFINITY, other = m2b != -INFINITY;
-    float ls = (own ? lsum[qb] * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
+    const float mnew = other ? fmaxf(m2[qb], m2b) : m2[qb];
+    const float a0 = __builtin_amdgcn_exp2f(m2[qb] - mnew);
+    const float a1 = other ? __builtin_amdgcn_exp2f(m2b - mnew) : 0.0f;
+    float ls = lsum[qb] * a0 + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
     ls = pair32_sum(ls);
     const float inv = 1.0f / ls;
     if (qi[qb] < a.Nq) {
@@ -286,7 +337,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const int e = e4 * 4 + q;
-            w[q] = ((own ? o[qb][b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
+            w[q] = (o[qb][b][e] * a0 + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
           }
           if (d < dh) *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
         }
@@ -294,62 +345,45 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   }
 }
 
-// One step of the online softmax for a 32-query block at head dim 64, where the row sum
-// is kept by vector adds. The scores arrive in exp2 units (q was multiplied by
-// scale * log2 e), and each lane's 16 of them become probabilities against the query's
-// offset m2: p = 2^(s - m2), added to the lane's row sum lsum and rounded to the bf16
-// P.V operands pf. The offset starts at 0 and is left alone while every row sum of the
-// block stays in [2^-64, 2^64]; while it is 0 for all queries of the wavefront the
-// subtraction is skipped (s - 0 is s: the same bits). A softmax does not depend on the
-// offset, and inside that range every probability, sum and output keeps its full
-// relative precision, so no max is taken at all in the usual case. When a sum leaves the
-// range (scores above about 64 or all below about -64 so far, non-finite scores), the
-// step takes the max over both lane halves and moves the offset: to the max, for a query
-// with no probability mass yet (which may lower it), else up to the max if that is
-// larger, with the accumulated output and sum rescaled; then the probabilities are
-// formed again. The offset is the same on both lane halves of a query at all times.
-template <int DB>
-__device__ __forceinline__ void softmax_step_sum(const f32x16& sc, float& m2, float& lsum, f32x16 (&o)[DB],
-                                                 bf16x8 (&pf)[2]) {
-  auto probs = [&](auto shifted) {
-    float l = lsum;
+// One step of the online softmax for QB 32-query blocks at head dim 64, where the row
+// sum is kept by vector adds (scores in exp2 units). The probabilities are formed
+// against the current offsets first (wave_probs) and added to the row sums; the offsets
+// start at 0 and are left alone while every row sum of a block stays in [2^-64, 2^64],
+// so the usual step takes no max at all. When a sum leaves the range (scores above
+// about 64 or all below about -64 so far, non-finite scores) that block takes the max
+// over both lane halves and moves the offset: to the max for a query with nothing
+// accumulated yet (which may lower it), else up to the max if that is larger, with the
+// output and sum rescaled; then its probabilities are formed again. A softmax does not
+// depend on the offset, and inside that range every probability, sum and output keeps
+// its relative precision. The offset is the same on both lane halves of a query.
+template <int QB, int DB>
+__device__ __forceinline__ void softmax_step_sum(const f32x16 (&sc)[QB], float (&m2)[QB], float (&lsum)[QB],
+                                                 f32x16 (&o)[QB][DB], bf16x8 (&pf)[QB][2]) {
+  float l[QB];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+  for (int qb = 0; qb < QB; ++qb) l[qb] = lsum[qb];
+  wave_probs<true>(sc, m2, l, pf);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float x = sc[ks * 8 + j];
-        const float p = __builtin_amdgcn_exp2f(decltype(shifted)::value ? x - m2 : x);
-        l += p;
-        pf[ks][j] = (bf16)p;
-      }
+  for (int qb = 0; qb < QB; ++qb) {
+    if (__any(!(l[qb] <= 0x1p64f && l[qb] >= 0x1p-64f))) {
+      float tmax = sc[qb][0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[qb][e]);
+      tmax = pair32_max(tmax);
+      const bool empty = pair32_sum(lsum[qb]) == 0.0f;  // nothing accumulated for this query yet
+      const float mnew = empty ? tmax : fmaxf(m2[qb], tmax);
+      const float alpha = empty ? 0.0f : __builtin_amdgcn_exp2f(m2[qb] - mnew);
+      lsum[qb] *= alpha;
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[qb][b][e] *= alpha;
+      m2[qb] = mnew;
+      l[qb] = lsum[qb];
+      block_probs<true, true>(sc[qb], m2[qb], l[qb], pf[qb]);
     }
-    return l;
-  };
-  float l = __all(m2 == 0.0f) ? probs(std::false_type{}) : probs(std::true_type{});
-  if (__any(!(l <= 0x1p64f && l >= 0x1p-64f))) {
-    float tmax = sc[0];
-#pragma unroll
-    for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[e]);
-    tmax = pair32_max(tmax);
-    const bool empty = pair32_sum(lsum) == 0.0f;  // nothing accumulated for this query yet
-    const float mnew = empty ? tmax : fmaxf(m2, tmax);
-    const float alpha = empty ? 0.0f : __builtin_amdgcn_exp2f(m2 - mnew);
-    lsum *= alpha;
-#pragma unroll
-    for (int b = 0; b < DB; ++b)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[b][e] *= alpha;
-    m2 = mnew;
-    l = probs(std::true_type{});
+    lsum[qb] = l[qb];
   }
-  lsum = l;
-}
-
-// q fragments of head dim 64 scaled into exp2 units: bf16(q * scale * log2 e), once per
-// wavefront, so the score MFMA returns the exponents the softmax takes.
-__device__ __forceinline__ void scale_q(bf16x8& q, float sl2) {
-#pragma unroll
-  for (int e = 0; e < 8; ++e) q[e] = (bf16)((float)q[e] * sl2);
 }
 
 // Head dim 64: the same computation with the K and V^T tiles moved by buffer_load ... lds
@@ -435,12 +469,13 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
       buffer_load16_lds(i < 2 ? k_src : v_src, sb + (i * 256 + wave * 64) * 16, goff[i]);
   };
 
-  f32x16 o[DB];
+  // one query block, held as arrays of one for the softmax helpers
+  f32x16 o[1][DB];
 #pragma unroll
   for (int b = 0; b < DB; ++b)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) o[b][e] = 0.0f;
-  float m2 = 0.0f, lsum = 0.0f;
+    for (int e = 0; e < 16; ++e) o[0][b][e] = 0.0f;
+  float m2[1] = {0.0f}, lsum[1] = {0.0f};
   const int sw = dma_swz<CPR>(l32);  // the swizzle of every row this lane reads
   const int krow = (kh * kKH + l32) * CPR;
 
@@ -454,25 +489,25 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
     const int kv0 = it * 2 * kKH + kh * kKH;
     // a key half wholly past the last key contributes nothing (see attn_bf16_kernel)
     if (kv0 >= a.Nk) return;
-    f32x16 sc;
+    f32x16 sc[1];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) sc[e] = 0.0f;
+    for (int e = 0; e < 16; ++e) sc[0][e] = 0.0f;
     // all K fragments are read before the first MFMA, so their LDS latencies overlap
     // (the compiler otherwise waits for each pair in turn)
     bf16x8 kf[DHC];
 #pragma unroll
     for (int kk = 0; kk < DHC; ++kk) kf[kk] = *(const bf16x8*)(cur + (krow + ((kk * 2 + g) ^ sw)) * 16);
 #pragma unroll
-    for (int kk = 0; kk < DHC; ++kk) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sc, 0, 0, 0);
+    for (int kk = 0; kk < DHC; ++kk) sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sc[0], 0, 0, 0);
     __builtin_amdgcn_sched_group_barrier(0x100, DHC, 0);  // LDS reads
     __builtin_amdgcn_sched_group_barrier(0x008, DHC, 0);  // then the MFMAs
     if (kv0 + kKH > a.Nk) {
 #pragma unroll
       for (int e = 0; e < 16; ++e)
-        if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) sc[e] = -INFINITY;
+        if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) sc[0][e] = -INFINITY;
     }
-    bf16x8 pf[2];
-    softmax_step_sum<DB>(sc, m2, lsum, o, pf);
+    bf16x8 pf[1][2];
+    softmax_step_sum(sc, m2, lsum, o, pf);
     // V^T fragment of k-slots 8g..8g+7: keys 16 ks + 4 g + 0..3 and 16 ks + 8 + 4 g + 0..3
     // of this half, which the permuted layout (vt_pos) keeps in one 16-byte chunk,
     // kh*4 + 2 ks + g
@@ -482,7 +517,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const bf16x8 vf = *(const bf16x8*)(vrow + (((kh * 4 + 2 * ks + g) ^ sw) << 4));
-        o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[b], 0, 0, 0);
+        o[0][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[0][ks], o[0][b], 0, 0, 0);
       }
     }
   };
@@ -509,9 +544,9 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
 #pragma unroll
     for (int b = 0; b < DB; ++b)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mg[(b * 16 + e) * 64 + lane] = o[b][e];
-    mg[DB * 16 * 64 + lane] = m2;
-    mg[(DB * 16 + 1) * 64 + lane] = lsum;
+      for (int e = 0; e < 16; ++e) mg[(b * 16 + e) * 64 + lane] = o[0][b][e];
+    mg[DB * 16 * 64 + lane] = m2[0];
+    mg[(DB * 16 + 1) * 64 + lane] = lsum[0];
   }
   __syncthreads();
   if (kh == 1) return;
@@ -519,12 +554,12 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   // zeros are then left out by selects, and its offset is not used)
   const bool other = kKH < a.Nk;
   const float m2b = mg[DB * 16 * 64 + lane];
-  const float mnew = other ? fmaxf(m2, m2b) : m2;
-  const float a0 = __builtin_amdgcn_exp2f(m2 - mnew);
+  const float mnew = other ? fmaxf(m2[0], m2b) : m2[0];
+  const float a0 = __builtin_amdgcn_exp2f(m2[0] - mnew);
   const float a1 = other ? __builtin_amdgcn_exp2f(m2b - mnew) : 0.0f;
-  lsum = lsum * a0 + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
-  lsum = pair32_sum(lsum);
-  const float inv = 1.0f / lsum;
+  float ls = lsum[0] * a0 + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
+  ls = pair32_sum(ls);
+  const float inv = 1.0f / ls;
   if (qi < a.Nq) {
     bf16* O = (bf16*)a.o + ((size_t)r * a.Nq + qi) * a.D + (size_t)head * DH;
 #pragma unroll
@@ -536,7 +571,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int e = e4 * 4 + q;
-          w[q] = (o[b][e] * a0 + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
+          w[q] = (o[0][b][e] * a0 + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
         }
         *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
       }
@@ -665,8 +700,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
           if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) sc[qb][e] = -INFINITY;
     }
     bf16x8 pf[QB][2];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) softmax_step_sum<DB>(sc[qb], m2[qb], lsum[qb], o[qb], pf[qb]);
+    softmax_step_sum(sc, m2, lsum, o, pf);
 #pragma unroll
     for (int b = 0; b < DB; ++b) {
       const char* vrow = cur + KCHUNKS * 16 + (b * 32 + l32) * CPR * 16;
@@ -810,6 +844,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
     *(u32x4*)(base + V_OFF + (row * 8 + c % 8) * 16) = u32x4{w, w, w, w};
   }
 
+  const float sl2 = a.scale * 1.4426950408889634f;
   bf16x8 qf[QB][DHC];
   const __amdgpu_buffer_rsrc_t q_src = buffer_rsrc(Q, (uint32_t)a.Nq * DH * 2);
 #pragma unroll
@@ -819,6 +854,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
       const int d0 = kk * 16 + g * 8;
       const u32x4 w = buffer_load16(q_src, (qi[qb] < a.Nq && d0 < DH) ? (qi[qb] * DH + d0) * 2 : kOffOOB);
       qf[qb][kk] = __builtin_bit_cast(bf16x8, w);
+      scale_q(qf[qb][kk], sl2);
     }
 
   // load i of a thread fills chunk position p = i * 256 + tid of a stage: K chunk p
@@ -863,10 +899,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
     for (int b = 0; b < DB; ++b)
 #pragma unroll
       for (int e = 0; e < 16; ++e) o[qb][b][e] = 0.0f;
-  float m2[QB];
+  float m2[QB], unused[QB];  // offsets; the row sums come from the ones row
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) m2[qb] = -INFINITY;
-  const float sl2 = a.scale * 1.4426950408889634f;
+  for (int qb = 0; qb < QB; ++qb) m2[qb] = unused[qb] = 0.0f;
   const int sw = dma_swz<8>(l32);
   const int krow = (kh * kKH + l32) * 9;
 
@@ -902,26 +937,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
           if (kv0 + (e >> 2) * 8 + g * 4 + (e & 3) >= a.Nk) sc[qb][e] = -INFINITY;
     }
     bf16x8 pf[QB][2];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      float tmax = sc[qb][0];
-#pragma unroll
-      for (int e = 1; e < 16; ++e) tmax = fmaxf(tmax, sc[qb][e]);
-      tmax = pair32_max(tmax) * sl2;
-      if (__any(tmax > m2[qb] + kLazy)) {
-        const float mnew = fmaxf(m2[qb], tmax);
-        const float alpha = __builtin_amdgcn_exp2f(m2[qb] - mnew);
-#pragma unroll
-        for (int b = 0; b < DB; ++b)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[qb][b][e] *= alpha;
-        m2[qb] = mnew;
-      }
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) pf[qb][ks][j] = (bf16)__builtin_amdgcn_exp2f(fmaf(sc[qb][ks * 8 + j], sl2, -m2[qb]));
-    }
+    softmax_step_lazy<false>(sc, it == 0, m2, unused, o, pf);
 #pragma unroll
     for (int b = 0; b < DB; ++b) {
       const char* vrow = cur + V_OFF + (b * 32 + l32) * 8 * 16;
@@ -970,12 +986,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
     }
     __syncthreads();
     if (kh == 1) continue;
+    // as in attn_bf16_kernel: half 1 saw keys only when there are more than 32
+    const bool other = kKH < a.Nk;
     const float m2b = mg[DB * 16 * 64 + lane];
-    const float mnew = fmaxf(m2[qb], m2b);
-    const float a0 = m2[qb] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2[qb] - mnew);
-    const float a1 = m2b == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m2b - mnew);
-    const bool own = m2[qb] != -INFINITY, other = m2b != -INFINITY;
-    float ls = (own ? lsum[qb] * a0 : 0.0f) + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
+    const float mnew = other ? fmaxf(m2[qb], m2b) : m2[qb];
+    const float a0 = __builtin_amdgcn_exp2f(m2[qb] - mnew);
+    const float a1 = other ? __builtin_amdgcn_exp2f(m2b - mnew) : 0.0f;
+    float ls = lsum[qb] * a0 + (other ? mg[(DB * 16 + 1) * 64 + lane] * a1 : 0.0f);
     ls = pair32_sum(ls);
     const float inv = 1.0f / ls;
     if (qi[qb] < a.Nq) {
@@ -989,7 +1006,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma72x2_kernel(AttnArgs a) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const int e = e4 * 4 + q;
-            w[q] = ((own ? o[qb][b][e] * a0 : 0.0f) + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
+            w[q] = (o[qb][b][e] * a0 + (other ? mg[(b * 16 + e) * 64 + lane] * a1 : 0.0f)) * inv;
           }
           if (d < DH) *(bf16x4*)(O + d) = bf16x4{(bf16)w[0], (bf16)w[1], (bf16)w[2], (bf16)w[3]};
         }
