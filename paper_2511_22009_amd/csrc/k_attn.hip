@@ -5,12 +5,12 @@
 //   * a workgroup owns 64 queries of one (row, head) and four wavefronts: two query
 //     groups of 32 times two key halves. Each step stages 64 keys; the first 32 go to
 //     the key-half-0 wavefronts, the next 32 to key-half-1, and the two halves' partial
-//     results (running max, sum, output) are merged at the end. Splitting the keys
+//     results (offset, sum, output) are merged at the end. Splitting the keys
 //     inside the workgroup gives 4 wavefronts per 64 queries, so a 512^2 layer (49152
 //     queries) is 768 workgroups, three per CU on 256 CUs;
 //   * scores are computed transposed, S^T = K Q^T, so the MFMA result gives each lane
-//     ONE query (column l%32) and 16 of the 32 keys of the block: the running max
-//     and sum are lane-local plus a single cross-half shuffle;
+//     ONE query (column l%32) and 16 of the 32 keys of the block: a step max and the
+//     sum are lane-local plus a single cross-half exchange;
 //   * q is scaled into exp2 units (times scale * log2 e, rounded to bf16) once per
 //     wavefront, and the probabilities 2^(s - m2) are formed against a per-query offset
 //     m2 that starts at 0: while it is 0 for the whole wavefront, a probability is one
@@ -251,8 +251,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     const bf16* Kb = Ks + (cur * 2 + kh) * KT;
     const bf16* Vb = Vs + (cur * 2 + kh) * VT;
     // a key half that lies wholly past the last key (key half 1 when Nk <= 32, or the
-    // tail of the last step) contributes nothing: its scores would all be -inf, and a
-    // wavefront that has seen no key yet would take exp2(-inf + inf)
+    // tail of the last step) contributes nothing and is skipped: its scores would all be
+    // -inf, and its step max would move the offset of a wavefront at its first step
     if (kv0 < a.Nk) {
       // every K and V^T fragment feeds the MFMAs of all QB query blocks
       f32x16 s[QB];
@@ -300,7 +300,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) lsum[qb] = o[qb][DB - 1][12];
   }
-  // merge the key halves one query block at a time: half 1 hands (o, max, partial sum)
+  // merge the key halves one query block at a time: half 1 hands (o, offset, partial sum)
   // to half 0 through LDS
   float* mg = (float*)smem + qg * 64 * (DB * 16 + 2);
 #pragma unroll
@@ -538,7 +538,7 @@ __global__ __launch_bounds__(256) void attn_bf16_dma64_kernel(AttnArgs a) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  // merge the key halves: half 1 hands (o, max, partial sum) to half 0 through LDS
+  // merge the key halves: half 1 hands (o, offset, partial sum) to half 0 through LDS
   float* mg = (float*)(qg == 0 ? st0 : st1);
   if (kh == 1) {
 #pragma unroll
@@ -728,7 +728,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_dma64x2_kernel(AttnArgs a) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  // merge the key halves one query block at a time: half 1 hands (o, max, partial sum)
+  // merge the key halves one query block at a time: half 1 hands (o, offset, partial sum)
   // to half 0 through LDS (stage 0 for query group 0, stage 1 for query group 1)
   float* mg = (float*)(qg == 0 ? st0 : st1);
 #pragma unroll
