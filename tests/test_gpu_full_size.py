@@ -196,6 +196,39 @@ def test_s1024_step_properties():
     np.testing.assert_array_equal(host(done), expect[-1])
 
 
+def test_s1024_attention_on_sampled_queries():
+    """Attention at the 1024^2 shape in the launch configuration the benchmark times (4
+    rows x 16 heads, 4096 queries and keys, head dim 72: the directly staged two-block
+    kernel), run alone through sf_attention on seeded bf16 q, k, v. 96 sampled (row, head,
+    query) outputs against fp64 softmax over all 4096 keys, element by element:
+    |got - ref| <= 2^-7 |ref| + 2^-6 rms(ref) (one bf16 rounding each of the output, of the
+    probabilities and of q times the softmax scale), plus relative L2 <= 1e-2."""
+    from helpers import elementwise_ratio
+    cfg = W.get_config("s1024")
+    m = model("s1024", "bf16", max_rows=cfg.rows)
+    R, H, N, dh, ldv = cfg.rows, cfg.heads, cfg.N, cfg.dh, m.info["vt_ld"]
+    rng = np.random.default_rng(1024)
+    q, k, v = (torch.from_numpy(rng.standard_normal((R, H, N, dh)).astype(np.float32)).to(torch.bfloat16)
+               for _ in range(3))
+    tok = np.arange(N)
+    col = (tok & ~12) | ((tok & 4) << 1) | ((tok & 8) >> 1)
+    vT = torch.zeros((R, H, dh, ldv), dtype=torch.bfloat16)
+    vT[..., torch.from_numpy(col)] = v.transpose(2, 3)
+    got = host(m.attention(q.cuda(), k.cuda(), vT.cuda()).float())  # [R, N, H * dh]
+    q64, k64, v64 = (a.float().numpy().astype(np.float64) for a in (q, k, v))
+    picks = rng.integers(0, [R, H, N], size=(96, 3))
+    got_s = np.stack([got[r, i, h * dh:(h + 1) * dh] for r, h, i in picks])
+    ref_s = []
+    for r, h, i in picks:
+        s = k64[r, h] @ q64[r, h, i] / np.sqrt(dh)
+        w = np.exp(s - s.max())
+        ref_s.append((w / w.sum()) @ v64[r, h])
+    ref_s = np.stack(ref_s)
+    ratio = elementwise_ratio(got_s, ref_s, 2.0 ** -7, 2.0 ** -6)
+    print("s1024 attention, 96 sampled queries: ratio", ratio, "relL2", rel_l2(got_s, ref_s))
+    assert ratio <= 1.0 and rel_l2(got_s, ref_s) <= 1e-2
+
+
 def test_s1024_full_depth_velocity_parity():
     """1024^2 (4096 tokens, 28 blocks, head dim 72) through the whole network and the
     output head, in the benchmark's launch configuration (all K slots in one call):
