@@ -74,8 +74,9 @@ def test_block0_intermediates(name, prec):
         assert worst[key] <= TOL[prec], worst
 
 
+@pytest.mark.parametrize("HW", [(32, 64), (10, 12), (8, 8)], ids=["512tok", "30tok", "16tok"])
 @pytest.mark.parametrize("D,heads", [(128, 2), (144, 2), (96, 2), (64, 2)], ids=["dh64", "dh72", "dh48", "dh32"])
-def test_attention_scores_far_from_zero(D, heads):
+def test_attention_scores_far_from_zero(D, heads, HW):
     """Scores whose level per query lies far outside [-64, 64] in exp2 units, on both
     sides: every key entry is 128 plus a small exact integer step, so a query's scores are
     a large offset (its product with the shared part, spread about +-185 exp2 units over
@@ -83,10 +84,12 @@ def test_attention_scores_far_from_zero(D, heads):
     offset, so the result is well conditioned, while the kernels' online softmax meets
     sums that overflow and underflow and maxima far from zero. bf16 attention alone
     (sf_attention) on exact bf16 inputs against the oracle's fp64 softmax: 64 rows run the
-    two-query-block kernels, four rows the one-block ones, and the four rows both ran
-    agree bit for bit."""
+    two-query-block kernels (where the grid is large enough for them), four rows the
+    one-block ones, and the four rows both ran agree bit for bit. At 30 and 16 tokens a
+    single step holds every key: the second key half sees none (16) or only part of its
+    keys (30), so the masked, partly empty step meets the offset moves too."""
     from paper_2511_22009_amd import Model, Precision
-    cfg = W.Config(f"attn{D}", C=4, H=32, W=64, p=2, D=D, L=1, heads=heads, mlp=128)
+    cfg = W.Config(f"attn{D}", C=4, H=HW[0], W=HW[1], p=2, D=D, L=1, heads=heads, mlp=128)
     m = Model(W.make_blob(cfg), Precision.BF16, 64)
     N, dh, ldv, R = cfg.N, D // heads, m.info["vt_ld"], 64
     rng = np.random.default_rng(91)
