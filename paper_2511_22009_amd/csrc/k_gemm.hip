@@ -381,13 +381,14 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
 // Block -> tile map. The hardware hands workgroup b to XCD b % 8 and each XCD has its
 // own L2, so each XCD gets a contiguous range of logical tiles; inside it tiles go in
 // groups of GM tile rows, M fastest, so the A rows and B columns a group touches are
-// reused from one L2. Bijective for any tile count. The QKV projection takes groups of
-// four (at 4096 x 2304 each XCD then owns four whole A row panels and every column
-// tile: 4 % faster there), the other GEMMs eight.
+// reused from one L2. Bijective for any tile count and group size. The QKV projection
+// takes groups of four where that measured faster (at 4096 x 2304 each XCD then owns
+// four whole A row panels and every column tile; also at 16384 rows), but not for 4096
+// rows of 128 x 128 tiles over 27 column tiles (width 1152), where eight are faster; the
+// other GEMMs take eight.
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
-template <int GM = kGroupM>
-__device__ __forceinline__ void tile_coords(int nbm, int nbn, int& mt, int& nt) {
+__device__ __forceinline__ void tile_coords(int nbm, int nbn, int& mt, int& nt, int GM = kGroupM) {
   const int T = nbm * nbn;
   const int b = blockIdx.x;
   const int xcd = b % kXcds, local = b / kXcds;
@@ -451,7 +452,10 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
   const int wm = wmn / WN, wn = wmn % WN;
   const int l32 = lane & 31, g = lane >> 5;
   int mt, nt;
-  tile_coords<KIND == EPI_QKV ? 4 : kGroupM>((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
+  {
+    const int nbm = (a.M + BM - 1) / BM, nbn = (a.N + BN - 1) / BN;
+    tile_coords(nbm, nbn, mt, nt, KIND == EPI_QKV && (nbm >= 64 || nbn <= 8) ? 4 : kGroupM);
+  }
   const int m0 = mt * BM, n0 = nt * BN;
   if (!tile_live<KIND, BM>(a, m0)) return;  // uniform across the workgroup
   // the tile's bias columns go to LDS now, so the epilogue does not wait on them
@@ -725,7 +729,7 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   const int wm = wmn / WN, wn = wmn % WN;
   const int l32 = lane & 31, g = lane >> 5;
   int mt, nt;
-  tile_coords<>((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
+  tile_coords((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
   if (!tile_live<KIND, BM>(a, m0)) return;  // uniform across the workgroup
   __shared__ __attribute__((aligned(16))) float bias_s[kBf16Out ? BN : 4];
