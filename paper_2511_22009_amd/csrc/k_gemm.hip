@@ -384,8 +384,8 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
 // reused from one L2. Bijective for any tile count and group size. The QKV projection
 // takes groups of four where that measured faster (at 4096 x 2304 each XCD then owns
 // four whole A row panels and every column tile; also at 16384 rows), but not for 4096
-// rows of 128 x 128 tiles over 27 column tiles (width 1152), where eight are faster; the
-// other GEMMs take eight.
+// rows of 128 x 128 tiles over 27 column tiles (width 1152), where eight are faster. The
+// MLP up-projection takes four on grids of at least 64 tile rows, the other GEMMs eight.
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 __device__ __forceinline__ void tile_coords(int nbm, int nbn, int& mt, int& nt, int GM = kGroupM) {
@@ -454,7 +454,8 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_sched_kernel(
   int mt, nt;
   {
     const int nbm = (a.M + BM - 1) / BM, nbn = (a.N + BN - 1) / BN;
-    tile_coords(nbm, nbn, mt, nt, KIND == EPI_QKV && (nbm >= 64 || nbn <= 8) ? 4 : kGroupM);
+    tile_coords(nbm, nbn, mt, nt,
+                (KIND == EPI_QKV && (nbm >= 64 || nbn <= 8)) || (KIND == EPI_GELU && nbm >= 64) ? 4 : kGroupM);
   }
   const int m0 = mt * BM, n0 = nt * BN;
   if (!tile_live<KIND, BM>(a, m0)) return;  // uniform across the workgroup
