@@ -385,7 +385,8 @@ __device__ __forceinline__ void bf16_epilogue(const GemmArgs& a, const f32x16 (&
 // takes groups of four where that measured faster (at 4096 x 2304 each XCD then owns
 // four whole A row panels and every column tile; also at 16384 rows), but not for 4096
 // rows of 128 x 128 tiles over 27 column tiles (width 1152), where eight are faster. The
-// MLP up-projection takes four on grids of at least 64 tile rows, the other GEMMs eight.
+// MLP up-projection, and the directly staged narrow GEMMs other than the MLP
+// down-projection, take four on grids of at least 64 tile rows; everything else eight.
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 __device__ __forceinline__ void tile_coords(int nbm, int nbn, int& mt, int& nt, int GM = kGroupM) {
@@ -730,7 +731,10 @@ __global__ __launch_bounds__(WM * WN * KSPLIT * 64) void gemm_bf16_dma_kernel(Ge
   const int wm = wmn / WN, wn = wmn % WN;
   const int l32 = lane & 31, g = lane >> 5;
   int mt, nt;
-  tile_coords((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, mt, nt);
+  {
+    const int nbm = (a.M + BM - 1) / BM, nbn = (a.N + BN - 1) / BN;
+    tile_coords(nbm, nbn, mt, nt, nbm >= 64 && KIND != EPI_RES_GATE_MLP ? 4 : kGroupM);
+  }
   const int m0 = mt * BM, n0 = nt * BN;
   if (!tile_live<KIND, BM>(a, m0)) return;  // uniform across the workgroup
   __shared__ __attribute__((aligned(16))) float bias_s[kBf16Out ? BN : 4];
