@@ -46,17 +46,17 @@ MI355X_HBM_GBS = 8000.0
 # only for the kernel sources it was measured on (hash below); otherwise traffic is null.
 KERNEL_SOURCES = ("k_gemm.hip", "k_attn.hip", "sf_device.h", "sf_launch.h")
 TRAFFIC = {
-    ("s512", "bf16", "FC2"): {"bytes": 94524987, "sources": "eb9651b1f805f31e",
+    ("s512", "bf16", "FC2"): {"bytes": 94525086, "sources": "cac1cfd0c9deab6b",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512", "bf16", "FC1"): {"bytes": 59994037, "sources": "eb9651b1f805f31e",
+    ("s512", "bf16", "FC1"): {"bytes": 59987705, "sources": "cac1cfd0c9deab6b",
                               "profile": "profiles/stream_step_s512_bf16_hbm_traffic.md"},
-    ("s512_large", "bf16", "FC2"): {"bytes": 187591162, "sources": "eb9651b1f805f31e",
+    ("s512_large", "bf16", "FC2"): {"bytes": 187609226, "sources": "cac1cfd0c9deab6b",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_large", "bf16", "FC1"): {"bytes": 134299587, "sources": "eb9651b1f805f31e",
+    ("s512_large", "bf16", "FC1"): {"bytes": 134056520, "sources": "cac1cfd0c9deab6b",
                                     "profile": "profiles/stream_step_s512_large_bf16.md"},
-    ("s512_cfg", "bf16", "FC2"): {"bytes": 386299374, "sources": "eb9651b1f805f31e",
+    ("s512_cfg", "bf16", "FC2"): {"bytes": 392050527, "sources": "cac1cfd0c9deab6b",
                                   "profile": "profiles/stream_step_s512_cfg_bf16.md"},
-    ("s1024", "bf16", "ATTN"): {"bytes": 161788529, "sources": "eb9651b1f805f31e",
+    ("s1024", "bf16", "ATTN"): {"bytes": 161797938, "sources": "cac1cfd0c9deab6b",
                                 "profile": "profiles/stream_step_s1024_bf16.md"},
 }
 
